@@ -1,0 +1,126 @@
+"""Pins of the reference planner: a hand-worked example, the partition and non-emptiness
+properties the workqueue must have (Sec. 3.3-3.4), the closed-form task count, and the
+counters the paper prints in Tab. 4."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import PlanParams, choose_split_count, ref_plan
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def test_hand_worked_example():
+    # T = 32, Hkv = 2, S forced to 2.
+    # lengths 0, 1, 33, 100, 64 -> tiles 0, 1, 2, 4, 2 -> nsplit 0, 1, 2, 2, 2
+    # row 1: tiles [0,1)            -> tokens [0,1)
+    # row 2: tiles [0,1) [1,2)      -> tokens [0,32) [32,33)
+    # row 3: tiles [0,2) [2,4)      -> tokens [0,64) [64,100)
+    # row 4: tiles [0,1) [1,2)      -> tokens [0,32) [32,64)
+    p = PlanParams(num_kv_heads=2, split_min=2, split_max=2)
+    tasks, offs, S = ref_plan([0, 1, 33, 100, 64], p)
+    assert S == 2
+    assert offs.tolist() == [0, 0, 1, 3, 5, 7]
+    expect = []
+    for (i, s, t0, t1) in [(1, 0, 0, 1), (2, 0, 0, 32), (2, 1, 32, 33), (3, 0, 0, 64),
+                           (3, 1, 64, 100), (4, 0, 0, 32), (4, 1, 32, 64)]:
+        for g in range(2):
+            expect.append([i, g, s, t0, t1])
+    assert tasks.tolist() == expect
+
+
+def test_balanced_bounds_three_splits_of_seven_tiles():
+    # 7 tiles over 3 splits: floor(s*7/3) = 0, 2, 4, 7 -> 2, 2, 3 tiles.
+    p = PlanParams(num_kv_heads=1, split_min=3, split_max=3)
+    tasks, _, _ = ref_plan([7 * 32 - 5], p)
+    assert tasks[:, 3:].tolist() == [[0, 64], [64, 128], [128, 219]]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_partition_properties(seed):
+    r = np.random.Generator(np.random.PCG64(seed))
+    B = int(r.integers(1, 12))
+    lens = r.integers(0, 5000, size=B)
+    lens[r.random(B) < 0.2] = 0
+    lo = int(r.integers(1, 8))
+    p = PlanParams(num_kv_heads=int(r.integers(1, 9)), split_min=lo, split_max=lo + int(r.integers(0, 40)),
+                   target_tasks=int(r.integers(1, 3000)))
+    tasks, offs, S = ref_plan(lens, p)
+    T = p.tile_tokens
+    assert p.split_min <= S <= p.split_max
+    # brute force over every (row, kv head): the tasks tile [0, N) in split order
+    for i, n in enumerate(lens):
+        tiles = -(-int(n) // T)
+        ns = offs[i + 1] - offs[i]
+        assert ns == min(S, tiles)
+        for g in range(p.num_kv_heads):
+            mine = [t for t in tasks.tolist() if t[0] == i and t[1] == g]
+            assert [t[2] for t in mine] == list(range(ns))
+            pos = 0
+            sizes = []
+            for (_, _, s, t0, t1) in mine:
+                assert t0 == pos and t1 > t0 and t0 % T == 0
+                assert t1 % T == 0 or t1 == n
+                sizes.append(-(-(t1 - t0) // T))
+                pos = t1
+            assert pos == n
+            if sizes:
+                assert max(sizes) - min(sizes) <= 1
+                assert max(sizes) == -(-tiles // ns)
+    # closed-form count and slot order (row, split, kv head) with kv head fastest
+    assert len(tasks) == p.num_kv_heads * sum(min(S, -(-int(n) // T)) for n in lens)
+    for k, (i, g, s, _, _) in enumerate(tasks.tolist()):
+        assert k == (offs[i] + s) * p.num_kv_heads + g
+
+
+def test_split_count_rule():
+    p = PlanParams()  # Hkv 8, bounds [16, 64], target 512
+    assert choose_split_count([32769], p) == 64            # 512 / 8 = 64
+    assert choose_split_count([1000] * 8, p) == 16         # 512 / 64 = 8 -> clamped up to 16
+    assert choose_split_count([1000] * 3 + [0] * 5, p) == 22  # ceil(512 / 24)
+    assert choose_split_count([0, 0], p) == 64             # no active row: 512 / max(1, 0)
+    assert choose_split_count([1] * 200, p) == 16
+
+
+def test_tiny_config_has_eight_tasks():
+    tasks, offs, S = ref_plan([512], PlanParams(split_min=1, split_max=1))
+    assert S == 1 and len(tasks) == 8 and offs.tolist() == [0, 1]
+    assert tasks[:, 3:].tolist() == [[0, 512]] * 8
+
+
+def test_b1_steps_give_512_tasks_and_a_17_tile_split():
+    p = PlanParams()
+    for n in range(32769, 32789):
+        tasks, _, S = ref_plan([n], p)
+        assert S == 64 and len(tasks) == 512
+        tiles = (tasks[:, 4] - tasks[:, 3] + 31) // 32
+        assert sorted(set(tiles.tolist())) == [16, 17]  # 1025 tiles over 64 splits
+
+
+def test_tab4_counters():
+    g = json.load(open(os.path.join(GOLDEN, "tab4_counters.json")))
+    G, d = g["shape"]["hq"] // g["shape"]["hkv"], g["shape"]["head_dim"]
+    state_bytes = 4 * (G * d + 2 * G)          # fp32 acc[G][d], m[G], l[G] per task
+    assert state_bytes == 2080
+    lens = [640, 700, 2000, 17000, 30000, 900, 25000, 32768]  # every row >= 20 tiles
+    wq = g["workqueue"]
+    tasks, _, S = ref_plan(lens, PlanParams(split_min=wq["split"], split_max=wq["split"]))
+    assert round(len(tasks) / g["sms"], 1) == wq["decode_cta_work_per_sm"]
+    assert round(len(tasks) * state_bytes / 2**20, 2) == wq["merge_mb"]
+    bk = g["buckets"]
+    slots = g["shape"]["batch"] * g["shape"]["hkv"] * bk["split"]   # rectangular grid
+    assert round(slots / g["sms"], 1) == bk["decode_cta_work_per_sm"]
+    assert round(slots * state_bytes / 2**20, 2) == bk["merge_mb"]
+
+
+def test_invalid_inputs_raise():
+    with pytest.raises(ValueError):
+        ref_plan([100], PlanParams(), max_pages_per_row=6)   # 6 pages hold 96 tokens
+    with pytest.raises(ValueError):
+        ref_plan([-1], PlanParams())
+    with pytest.raises(ValueError):
+        ref_plan([10], PlanParams(tile_tokens=24))
+    with pytest.raises(ValueError):
+        ref_plan([10], PlanParams(split_min=5, split_max=4))
