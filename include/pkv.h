@@ -1,0 +1,167 @@
+/*
+ * pkv: paged grouped-query decode attention for MI355X (gfx950).
+ *
+ * C ABI of libpkv.so. One decode step is
+ *
+ *     pkv_plan   : seq_lens -> compact task list + split_offsets       (one kernel)
+ *     pkv_decode : tasks, Q, paged K/V -> out                          (one fused kernel,
+ *                                                                       or split + merge)
+ *
+ * The operation is single-token decode attention, Eq. (1) of the paper, with grouped
+ * query heads (Sec. 3.1): query head h reads KV head h / G, G = Hq / Hkv. K and V are
+ * read in place through a block table (Sec. 3.2). The sequence is cut into splits whose
+ * online-softmax partial states are merged exactly (Sec. 3.3), and the workqueue holds
+ * only non-empty (row, KV head, split) tasks (Sec. 3.4).
+ *
+ * Conventions shared by every call:
+ *  - Device pointers are HIP device memory owned by the caller. The library never
+ *    allocates or frees memory and never synchronizes, except pkv_check_device_status.
+ *  - All work is enqueued on `stream` and is asynchronous. A nonzero return means
+ *    nothing was enqueued.
+ *  - Tensors are row-major and contiguous; fp16 buffers hold IEEE binary16 bit patterns
+ *    (uint16_t) and the arithmetic is fp32.
+ *  - Host-side validation returns a status synchronously. Faults found on the device
+ *    (a page id outside the pool, a length beyond the block table) set bits in the
+ *    workspace's error word, read back by pkv_check_device_status, and the affected
+ *    rows' outputs are written as zeros.
+ *  - Concurrent calls on different streams need separate workspaces.
+ */
+#ifndef PKV_H
+#define PKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define PKV_OK 0
+#define PKV_ERR_INVALID_ARG 1 /* null pointer, non-positive size, Hq % Hkv != 0, bad bounds */
+#define PKV_ERR_UNSUPPORTED 2 /* d != 128, page_size != 16, G not in {1,2,4,8}, tile not a page multiple */
+#define PKV_ERR_WORKSPACE 3   /* workspace, max_tasks or a split count too small */
+#define PKV_ERR_HIP 4         /* a HIP runtime call or kernel launch failed */
+#define PKV_ERR_DEVICE 5      /* pkv_check_device_status found device error bits */
+
+/* Device error bits (pkv_check_device_status). */
+#define PKV_DEVERR_SEQ_LEN 1u /* seq_len < 0 or > max_pages_per_row * page_size: row dropped */
+#define PKV_DEVERR_PAGE_ID 2u /* block_table entry outside [0, num_pages): row's output zeroed */
+#define PKV_DEVERR_TASK 4u    /* a task outside the batch or its row's block table: skipped;
+                                 outputs are unspecified unless the task list came from
+                                 pkv_plan for the same seq_lens */
+
+/* pkv_decode flags. */
+#define PKV_FUSED_MERGE 1 /* merge in the split kernel by the last-arriving split (Sec. 3.4) */
+
+/* One workqueue task (Sec. 3.4): KV head `kvh` of batch row `row`, split `split`,
+ * tokens [t_begin, t_end) of that row. 20 bytes, tightly packed. */
+typedef struct {
+  int32_t row, kvh, split, t_begin, t_end;
+} pkv_task;
+
+/* Planner parameters (host struct).
+ *   page_size    tokens per KV page; must be 16
+ *   tile_tokens  split granularity in tokens (the paper's 32-token tile, Sec. 3.2);
+ *                a positive multiple of page_size
+ *   num_kv_heads Hkv
+ *   split_min, split_max  bounds on the split count S, 1 <= split_min <= split_max
+ *   target_tasks S = clamp(ceil(target_tasks / max(1, B_active * Hkv)), split_min,
+ *                split_max), B_active = rows with seq_len > 0 (Sec. 3.5: the workqueue
+ *                split count follows the active batch size); target_tasks >= 1 */
+typedef struct {
+  int32_t page_size;
+  int32_t tile_tokens;
+  int32_t num_kv_heads;
+  int32_t split_min;
+  int32_t split_max;
+  int32_t target_tasks;
+} pkv_plan_params;
+
+/* Upper bound on the task count of any plan: B * Hkv * split_max. Returns -1 on a
+ * non-positive argument or int32 overflow. */
+int32_t pkv_max_tasks(int32_t B, int32_t Hkv, int32_t split_max);
+
+/* Bytes of workspace for batches of up to B rows and up to max_tasks partial-state
+ * slots: a 256-byte header (error word), B*Hkv completion counters, and max_tasks
+ * slots of fp32 {m[G], l[G], acc[G][d]} (2080 bytes at G=4, d=128). Returns 0 on a
+ * bad argument. The rectangular route needs max_tasks >= B * Hkv * S. */
+size_t pkv_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_tasks);
+
+/* Zero the workspace header and completion counters (enqueued on `stream`). Call once
+ * after allocating a workspace; afterwards the library keeps the counters at zero
+ * between calls and the error word is cleared by pkv_check_device_status. */
+int pkv_workspace_init(void* ws, size_t ws_bytes, int32_t B, int32_t Hkv, hipStream_t stream);
+
+/* Build the compact workqueue of Sec. 3.4 on the device (one kernel).
+ *   seq_lens      device int32 [B]: N*_i, the row-local lengths (Sec. 3.3)
+ *   block_table   device int32 [B, max_pages_per_row] or NULL; when given, the entries
+ *                 each row uses are checked against [0, num_pages) and a row with a bad
+ *                 entry gets PKV_DEVERR_PAGE_ID (pkv_decode checks them in any case)
+ *   params        host pointer, see pkv_plan_params
+ *   tasks         device pkv_task [max_tasks]; entries [0, *num_tasks) are written in
+ *                 (row, split, kvh) order, kvh fastest; task k's partial state lives in
+ *                 slot k = (split_offsets[row] + split) * Hkv + kvh
+ *   split_offsets device int32 [B+1]: split_offsets[i+1] - split_offsets[i] = splits of
+ *                 row i = min(S, ceil(seq_len_i / tile_tokens))
+ *   num_tasks     device int32 [1]
+ *   ws            workspace of at least pkv_workspace_size(B, ., Hkv, ., 0) bytes; the
+ *                 plan zeroes the completion counters
+ * max_tasks must be >= pkv_max_tasks(B, Hkv, split_max). B <= 4096. Rows whose
+ * seq_len is out of range are planned as empty and flagged (PKV_DEVERR_SEQ_LEN). */
+int pkv_plan(const int32_t* seq_lens, const int32_t* block_table, int32_t B,
+             int32_t max_pages_per_row, int32_t num_pages, const pkv_plan_params* params,
+             pkv_task* tasks, int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks,
+             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Decode attention over the task list (Sec. 3.3-3.4).
+ *   q          device fp16 [B, Hq, d]
+ *   k_cache, v_cache  device fp16 [num_pages, page_size=16, Hkv, d] (token-major pages)
+ *   block_table device int32 [B, max_pages_per_row]: logical page -> physical page
+ *   seq_lens   device int32 [B]
+ *   tasks, split_offsets, num_tasks  as written by pkv_plan for the same seq_lens
+ *   max_tasks  capacity used by that plan (bounds the launch)
+ *   sm_scale   softmax scale (1/sqrt(d) of Eq. 1 unless Q is pre-scaled)
+ *   flags      0: split kernel + merge kernel; PKV_FUSED_MERGE: one kernel in which the
+ *              last split of each (row, KV head) to finish merges, in split order
+ *   out        device fp16 [B, Hq, d]; rows with seq_len 0 are written as zeros
+ *   ws         workspace of at least pkv_workspace_size(B, Hq, Hkv, d, max_tasks) bytes
+ * Both flag values give bit-identical outputs. Supported: d = 128, G in {1,2,4,8}. */
+int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+               int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+               const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+               const pkv_task* tasks, const int32_t* split_offsets, const int32_t* num_tasks,
+               int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out, void* ws,
+               size_t ws_bytes, hipStream_t stream);
+
+/* Rectangular split grid (Sec. 3.4): B * Hkv * S split workgroups, then a merge over
+ * all S columns (two kernels, no planner). Column s of row i owns the same balanced
+ * tile range the planner gives split s when s < min(S, tiles_i); otherwise it writes
+ * the neutral state (-inf, 0, 0) and exits before loading Q (Sec. 3.3). With the same
+ * S the output is bit-identical to pkv_decode. ws needs max_tasks >= B * Hkv * S;
+ * tile_tokens as in pkv_plan_params. */
+int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                    int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                    const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                    int32_t S, int32_t tile_tokens, float sm_scale, uint16_t* out, void* ws,
+                    size_t ws_bytes, hipStream_t stream);
+
+/* Synchronize `stream`, read the workspace error word into *error_bits (may be NULL)
+ * and clear it. Returns PKV_OK when no bit was set, PKV_ERR_DEVICE otherwise. */
+int pkv_check_device_status(void* ws, hipStream_t stream, uint32_t* error_bits);
+
+/* Static text for a status code. */
+const char* pkv_status_string(int status);
+
+/* Streaming copy of `bytes` (a multiple of 16) from src to dst on `stream`: the
+ * bandwidth probe used to calibrate HBM traffic counters and to evict the last-level
+ * cache between timed steps. */
+int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PKV_H */

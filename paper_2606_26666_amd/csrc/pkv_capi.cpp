@@ -1,0 +1,199 @@
+// C ABI of libpkv.so: argument validation, workspace layout and kernel launches.
+// Every check here runs on the host before anything is enqueued, so a rejected call
+// leaves the stream untouched.
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "pkv_internal.h"
+
+using namespace pkv;
+
+namespace {
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int from_hip(hipError_t e) { return e == hipSuccess ? PKV_OK : PKV_ERR_HIP; }
+
+int check_heads(int32_t Hq, int32_t Hkv, int32_t d, int* G) {
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return PKV_ERR_INVALID_ARG;
+  if (d != kHeadDim) return PKV_ERR_UNSUPPORTED;
+  const int g = Hq / Hkv;
+  if (g != 1 && g != 2 && g != 4 && g != 8) return PKV_ERR_UNSUPPORTED;
+  *G = g;
+  return PKV_OK;
+}
+
+int check_pool(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t num_pages,
+               const int32_t* bt, int32_t maxp, const int32_t* seq_lens, int32_t B, uint16_t* out,
+               void* ws) {
+  if (!q || !k || !v || !bt || !seq_lens || !out || !ws) return PKV_ERR_INVALID_ARG;
+  if (B < 1 || num_pages < 1 || maxp < 1) return PKV_ERR_INVALID_ARG;
+  if ((int64_t)maxp * kPageSize > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  // 16-byte vector loads of Q/K/V, 4-byte output stores, 16-byte workspace rows
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 4) || !aligned(ws, 16))
+    return PKV_ERR_INVALID_ARG;
+  return PKV_OK;
+}
+
+DecodeArgs make_args(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t num_pages,
+                     const int32_t* bt, int32_t maxp, const int32_t* seq_lens, int32_t B, int32_t Hq,
+                     int32_t Hkv, float sm_scale, uint16_t* out, void* ws) {
+  DecodeArgs a;
+  std::memset(&a, 0, sizeof(a));
+  char* w = static_cast<char*>(ws);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.block_table = bt;
+  a.seq_lens = seq_lens;
+  a.out = out;
+  a.err = reinterpret_cast<unsigned*>(w);
+  a.counters = reinterpret_cast<int32_t*>(w + kWsHeaderBytes);
+  a.partials = reinterpret_cast<float*>(w + partials_offset(B, Hkv));
+  a.num_pages = num_pages;
+  a.max_pages_per_row = maxp;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.scale_log2 = (float)((double)sm_scale * 1.4426950408889634);  // log2(e)
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t pkv_max_tasks(int32_t B, int32_t Hkv, int32_t split_max) {
+  if (B < 1 || Hkv < 1 || split_max < 1) return -1;
+  const int64_t n = (int64_t)B * Hkv * split_max;
+  return n > INT32_MAX ? -1 : (int32_t)n;
+}
+
+size_t pkv_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_tasks) {
+  int G = 0;
+  if (B < 1 || max_tasks < 0 || check_heads(Hq, Hkv, d, &G) != PKV_OK) return 0;
+  return partials_offset(B, Hkv) + (size_t)max_tasks * slot_floats(G) * sizeof(float);
+}
+
+int pkv_workspace_init(void* ws, size_t ws_bytes, int32_t B, int32_t Hkv, hipStream_t stream) {
+  if (!ws || B < 1 || Hkv < 1 || !aligned(ws, 16)) return PKV_ERR_INVALID_ARG;
+  const size_t n = partials_offset(B, Hkv);
+  if (ws_bytes < n) return PKV_ERR_WORKSPACE;
+  return from_hip(launch_zero(ws, n, stream));
+}
+
+int pkv_plan(const int32_t* seq_lens, const int32_t* block_table, int32_t B, int32_t max_pages_per_row,
+             int32_t num_pages, const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+             int32_t* split_offsets, int32_t* num_tasks, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!seq_lens || !params || !tasks || !split_offsets || !num_tasks || !ws) return PKV_ERR_INVALID_ARG;
+  if (B < 1 || B > kMaxPlanBatch || max_pages_per_row < 1) return PKV_ERR_INVALID_ARG;
+  if (block_table && num_pages < 1) return PKV_ERR_INVALID_ARG;
+  if (!aligned(ws, 16) || !aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
+  const pkv_plan_params p = *params;
+  if (p.page_size != kPageSize) return PKV_ERR_UNSUPPORTED;
+  if (p.tile_tokens <= 0 || p.tile_tokens % p.page_size != 0) return PKV_ERR_UNSUPPORTED;
+  if (p.num_kv_heads < 1 || p.split_min < 1 || p.split_min > p.split_max || p.target_tasks < 1)
+    return PKV_ERR_INVALID_ARG;
+  if ((int64_t)max_pages_per_row * p.page_size > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  const int32_t bound = pkv_max_tasks(B, p.num_kv_heads, p.split_max);
+  if (bound < 0) return PKV_ERR_INVALID_ARG;
+  if (max_tasks < bound) return PKV_ERR_WORKSPACE;
+  if (ws_bytes < partials_offset(B, p.num_kv_heads)) return PKV_ERR_WORKSPACE;
+  PlanArgs a;
+  a.seq_lens = seq_lens;
+  a.block_table = block_table;
+  a.B = B;
+  a.max_pages_per_row = max_pages_per_row;
+  a.num_pages = num_pages;
+  a.page_size = p.page_size;
+  a.tile_tokens = p.tile_tokens;
+  a.Hkv = p.num_kv_heads;
+  a.split_min = p.split_min;
+  a.split_max = p.split_max;
+  a.target_tasks = p.target_tasks;
+  a.tasks = tasks;
+  a.max_tasks = max_tasks;
+  a.split_offsets = split_offsets;
+  a.num_tasks = num_tasks;
+  a.err = reinterpret_cast<unsigned*>(ws);
+  a.counters = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kWsHeaderBytes);
+  return from_hip(launch_plan(a, stream));
+}
+
+int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+               const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
+               int32_t Hq, int32_t Hkv, int32_t d, const pkv_task* tasks, const int32_t* split_offsets,
+               const int32_t* num_tasks, int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out,
+               void* ws, size_t ws_bytes, hipStream_t stream) {
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
+  if (st != PKV_OK) return st;
+  if (!tasks || !split_offsets || !num_tasks || !aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
+  int G = 0;
+  if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
+  if (flags != 0 && flags != PKV_FUSED_MERGE) return PKV_ERR_INVALID_ARG;
+  if (!std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
+  if (max_tasks < 1) return PKV_ERR_INVALID_ARG;
+  if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, max_tasks)) return PKV_ERR_WORKSPACE;
+  DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
+                           Hkv, sm_scale, out, ws);
+  a.tasks = tasks;
+  a.split_offsets = split_offsets;
+  a.num_tasks = num_tasks;
+  a.max_tasks = max_tasks;
+  // one workgroup per possible task; those past *num_tasks exit at once
+  return from_hip(launch_decode(a, G, flags == PKV_FUSED_MERGE ? 1 : 0, max_tasks, stream));
+}
+
+int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                    const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
+                    int32_t Hq, int32_t Hkv, int32_t d, int32_t S, int32_t tile_tokens, float sm_scale,
+                    uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
+  if (st != PKV_OK) return st;
+  int G = 0;
+  if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
+  if (S < 1 || !std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
+  if (tile_tokens <= 0 || tile_tokens % kPageSize != 0) return PKV_ERR_UNSUPPORTED;
+  const int32_t slots = pkv_max_tasks(B, Hkv, S);
+  if (slots < 0) return PKV_ERR_INVALID_ARG;
+  if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, slots)) return PKV_ERR_WORKSPACE;
+  DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
+                           Hkv, sm_scale, out, ws);
+  a.S = S;
+  a.tile_tokens = tile_tokens;
+  a.max_tasks = slots;
+  return from_hip(launch_decode(a, G, 2, slots, stream));
+}
+
+int pkv_check_device_status(void* ws, hipStream_t stream, uint32_t* error_bits) {
+  if (!ws) return PKV_ERR_INVALID_ARG;
+  if (hipStreamSynchronize(stream) != hipSuccess) return PKV_ERR_HIP;
+  uint32_t bits = 0;
+  if (hipMemcpy(&bits, ws, sizeof(bits), hipMemcpyDeviceToHost) != hipSuccess) return PKV_ERR_HIP;
+  if (launch_zero(ws, sizeof(uint32_t), stream) != hipSuccess) return PKV_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return PKV_ERR_HIP;
+  if (error_bits) *error_bits = bits;
+  return bits ? PKV_ERR_DEVICE : PKV_OK;
+}
+
+const char* pkv_status_string(int status) {
+  switch (status) {
+    case PKV_OK: return "ok";
+    case PKV_ERR_INVALID_ARG: return "invalid argument";
+    case PKV_ERR_UNSUPPORTED: return "unsupported shape or parameter";
+    case PKV_ERR_WORKSPACE: return "workspace or task capacity too small";
+    case PKV_ERR_HIP: return "HIP runtime error";
+    case PKV_ERR_DEVICE: return "device-side error flagged";
+    default: return "unknown status";
+  }
+}
+
+int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+  if (!src || !dst || bytes % 16 != 0 || !aligned(src, 16) || !aligned(dst, 16)) return PKV_ERR_INVALID_ARG;
+  return from_hip(launch_copy(src, dst, bytes, stream));
+}
+
+}  // extern "C"

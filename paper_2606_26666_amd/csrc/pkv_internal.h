@@ -1,0 +1,63 @@
+// Internal interface between the C ABI (pkv_capi.cpp) and the kernels (pkv_kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/pkv.h"
+
+namespace pkv {
+
+constexpr int kHeadDim = 128;
+constexpr int kPageSize = 16;
+constexpr int kMaxPlanBatch = 4096;
+constexpr size_t kWsHeaderBytes = 256;
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline size_t slot_floats(int G) { return size_t(2 * G + G * kHeadDim); }
+inline size_t counters_bytes(int B, int Hkv) { return align256(size_t(B) * size_t(Hkv) * 4); }
+inline size_t partials_offset(int B, int Hkv) { return kWsHeaderBytes + counters_bytes(B, Hkv); }
+
+struct DecodeArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* block_table;
+  const int32_t* seq_lens;
+  const pkv_task* tasks;
+  const int32_t* split_offsets;
+  const int32_t* num_tasks;
+  uint16_t* out;
+  unsigned* err;
+  int32_t* counters;
+  float* partials;
+  int32_t num_pages;
+  int32_t max_pages_per_row;
+  int32_t B, Hq, Hkv;
+  int32_t max_tasks;
+  int32_t S;            // rectangular route only
+  int32_t tile_tokens;  // rectangular route only
+  float scale_log2;     // sm_scale * log2(e)
+};
+
+struct PlanArgs {
+  const int32_t* seq_lens;
+  const int32_t* block_table;
+  int32_t B, max_pages_per_row, num_pages;
+  int32_t page_size, tile_tokens, Hkv, split_min, split_max, target_tasks;
+  pkv_task* tasks;
+  int32_t max_tasks;
+  int32_t* split_offsets;
+  int32_t* num_tasks;
+  unsigned* err;
+  int32_t* counters;
+};
+
+hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
+// mode: 0 split + merge kernels, 1 fused merge, 2 rectangular split + merge
+hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s);
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+
+}  // namespace pkv

@@ -1,0 +1,131 @@
+"""The C ABI library loads, exports every function include/pkv.h declares, sizes its
+buffers as documented, and rejects bad arguments on the host before enqueuing anything
+(no GPU needed: every call below fails validation, so no HIP call is made)."""
+import ctypes
+
+import pytest
+
+import paper_2606_26666_amd as pkv
+from paper_2606_26666_amd import _binding as b
+
+FAKE = 4096  # a non-null, 16-byte-aligned address that is never dereferenced
+
+
+def lib():
+    try:
+        return pkv.lib()
+    except RuntimeError as e:  # the build step has not run
+        pytest.fail(str(e))
+
+
+def test_exports_every_header_function():
+    L = lib()
+    names = pkv.header_functions()
+    assert {"pkv_plan", "pkv_decode", "pkv_decode_rect", "pkv_max_tasks", "pkv_workspace_size",
+            "pkv_workspace_init", "pkv_check_device_status", "pkv_status_string", "pkv_stream_copy"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_sizes():
+    assert pkv.pkv_max_tasks(1, 8, 64) == 512
+    assert pkv.pkv_max_tasks(8, 8, 64) == 4096
+    assert pkv.pkv_max_tasks(0, 8, 64) == -1
+    assert pkv.pkv_max_tasks(1 << 20, 1 << 10, 1 << 10) == -1
+    # header 256 + counters (8 -> 256) + 512 slots of fp32 {m[4], l[4], acc[4][128]} = 2080 B
+    assert pkv.pkv_workspace_size(1, 32, 8, 128, 512) == 256 + 256 + 512 * 2080
+    assert pkv.pkv_workspace_size(8, 32, 8, 128, 10) == 256 + 256 + 10 * 2080
+    assert pkv.pkv_workspace_size(1, 8, 8, 128, 1) == 512 + 4 * (2 + 128)
+    assert pkv.pkv_workspace_size(1, 32, 8, 64, 1) == 0      # d != 128
+    assert pkv.pkv_workspace_size(1, 30, 8, 128, 1) == 0     # Hq % Hkv
+    assert pkv.pkv_workspace_size(1, 64, 4, 128, 1) == 0     # G = 16 has no kernel
+
+
+def test_status_strings():
+    L = lib()
+    for st in range(6):
+        assert L.pkv_status_string(st)
+    assert L.pkv_status_string(99) == b"unknown status"
+
+
+def plan(L, **kw):
+    args = dict(seq_lens=FAKE, bt=0, B=2, maxp=10, num_pages=100,
+                params=b.PlanParams(16, 32, 8, 16, 64, 512), tasks=FAKE, max_tasks=2 * 8 * 64,
+                offs=FAKE, ntasks=FAKE, ws=FAKE, ws_bytes=1 << 20)
+    args.update(kw)
+    return L.pkv_plan(args["seq_lens"], args["bt"], args["B"], args["maxp"], args["num_pages"],
+                      ctypes.byref(args["params"]), args["tasks"], args["max_tasks"], args["offs"],
+                      args["ntasks"], args["ws"], args["ws_bytes"], None)
+
+
+def test_plan_validation():
+    L = lib()
+    assert plan(L, seq_lens=0) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, tasks=0) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, B=0) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, B=5000, max_tasks=5000 * 8 * 64) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, maxp=0) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, bt=FAKE, num_pages=0) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, ws=FAKE + 4) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, params=b.PlanParams(8, 32, 8, 16, 64, 512)) == pkv.PKV_ERR_UNSUPPORTED
+    assert plan(L, params=b.PlanParams(16, 24, 8, 16, 64, 512)) == pkv.PKV_ERR_UNSUPPORTED
+    assert plan(L, params=b.PlanParams(16, 0, 8, 16, 64, 512)) == pkv.PKV_ERR_UNSUPPORTED
+    assert plan(L, params=b.PlanParams(16, 32, 8, 65, 64, 512)) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, params=b.PlanParams(16, 32, 8, 0, 64, 512)) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, params=b.PlanParams(16, 32, 0, 16, 64, 512)) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, params=b.PlanParams(16, 32, 8, 16, 64, 0)) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, max_tasks=2 * 8 * 64 - 1) == pkv.PKV_ERR_WORKSPACE
+    assert plan(L, ws_bytes=511) == pkv.PKV_ERR_WORKSPACE
+    assert plan(L, maxp=1 << 28) == pkv.PKV_ERR_INVALID_ARG
+
+
+def decode(L, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, num_pages=100, bt=FAKE, maxp=10, seq_lens=FAKE, B=2, Hq=32, Hkv=8, d=128,
+             tasks=FAKE, offs=FAKE, ntasks=FAKE, max_tasks=1024, scale=1.0, flags=1, out=FAKE, ws=FAKE,
+             ws_bytes=1 << 22)
+    a.update(kw)
+    return L.pkv_decode(a["q"], a["k"], a["v"], a["num_pages"], a["bt"], a["maxp"], a["seq_lens"], a["B"],
+                        a["Hq"], a["Hkv"], a["d"], a["tasks"], a["offs"], a["ntasks"], a["max_tasks"],
+                        a["scale"], a["flags"], a["out"], a["ws"], a["ws_bytes"], None)
+
+
+def test_decode_validation():
+    L = lib()
+    for k in ("q", "k", "v", "bt", "seq_lens", "tasks", "offs", "ntasks", "out", "ws"):
+        assert decode(L, **{k: 0}) == pkv.PKV_ERR_INVALID_ARG, k
+    assert decode(L, q=FAKE + 2) == pkv.PKV_ERR_INVALID_ARG       # 16-byte alignment
+    assert decode(L, out=FAKE + 2) == pkv.PKV_ERR_INVALID_ARG
+    assert decode(L, B=0) == pkv.PKV_ERR_INVALID_ARG
+    assert decode(L, num_pages=0) == pkv.PKV_ERR_INVALID_ARG
+    assert decode(L, Hq=30) == pkv.PKV_ERR_INVALID_ARG
+    assert decode(L, d=64) == pkv.PKV_ERR_UNSUPPORTED
+    assert decode(L, Hq=64, Hkv=4) == pkv.PKV_ERR_UNSUPPORTED     # G = 16
+    assert decode(L, Hq=24, Hkv=8) == pkv.PKV_ERR_UNSUPPORTED     # G = 3
+    assert decode(L, flags=3) == pkv.PKV_ERR_INVALID_ARG
+    assert decode(L, scale=float("nan")) == pkv.PKV_ERR_INVALID_ARG
+    assert decode(L, max_tasks=0) == pkv.PKV_ERR_INVALID_ARG
+    assert decode(L, ws_bytes=1000) == pkv.PKV_ERR_WORKSPACE
+
+
+def test_rect_validation():
+    L = lib()
+
+    def rect(**kw):
+        a = dict(q=FAKE, S=16, tile=32, ws_bytes=1 << 22, B=2, d=128)
+        a.update(kw)
+        return L.pkv_decode_rect(a["q"], FAKE, FAKE, 100, FAKE, 10, FAKE, a["B"], 32, 8, a["d"], a["S"],
+                                 a["tile"], 1.0, FAKE, FAKE, a["ws_bytes"], None)
+    assert rect(S=0) == pkv.PKV_ERR_INVALID_ARG
+    assert rect(tile=24) == pkv.PKV_ERR_UNSUPPORTED
+    assert rect(d=96) == pkv.PKV_ERR_UNSUPPORTED
+    assert rect(q=0) == pkv.PKV_ERR_INVALID_ARG
+    assert rect(ws_bytes=2 * 8 * 16 * 2080) == pkv.PKV_ERR_WORKSPACE  # header missing
+
+
+def test_copy_and_init_validation():
+    L = lib()
+    assert L.pkv_stream_copy(FAKE, FAKE, 15, None) == pkv.PKV_ERR_INVALID_ARG
+    assert L.pkv_stream_copy(0, FAKE, 16, None) == pkv.PKV_ERR_INVALID_ARG
+    assert L.pkv_workspace_init(FAKE, 100, 1, 8, None) == pkv.PKV_ERR_WORKSPACE
+    assert L.pkv_workspace_init(0, 1 << 20, 1, 8, None) == pkv.PKV_ERR_INVALID_ARG
+    assert L.pkv_check_device_status(0, None, None) == pkv.PKV_ERR_INVALID_ARG

@@ -1,0 +1,219 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Bars: the task list is bit-exact against ref_plan; outputs are within max abs 2e-3 and
+normwise rel 1e-2 of ref_decode; routes that must agree bitwise (fused vs two-kernel
+merge, workqueue vs rectangular grid at the same split count, physical page
+permutation, one-token context) are compared with torch.equal. Unowned pool pages and
+the partial-state workspace are NaN before every call, so a stray read or an
+unwritten slot shows up."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_26666_amd as pkv
+from oracle import PlanParams, ref_decode, ref_decode_rect, ref_plan
+from tests.gpu_cases import (Case, assert_close, plan_params, read_plan, run_decode, run_plan, run_rect,
+                             ulp_fraction)
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = [1, 15, 16, 17, 31, 32, 33, 100, 517, 1000, 2049, 0, 4000]
+
+
+def bufs_for(case, split_max=64, rect_splits=0):
+    return pkv.DecodeBuffers(case.B, case.hq, case.hkv, case.d, split_max, "cuda", rect_splits=rect_splits)
+
+
+def oracle_plan(case, p):
+    return ref_plan(case.lens, PlanParams(p.page_size, p.tile_tokens, p.num_kv_heads, p.split_min, p.split_max,
+                                          p.target_tasks), max_pages_per_row=case.bt.shape[1])
+
+
+@pytest.mark.parametrize("smin,smax,target", [(16, 64, 512), (1, 1, 512), (2, 7, 100), (3, 64, 4096)])
+def test_plan_bit_exact_ragged(smin, smax, target):
+    case = Case(RAGGED, seed=1)
+    p = plan_params(8, smin, smax, target)
+    bufs = bufs_for(case, smax)
+    run_plan(case, bufs, p, check_pages=True)
+    tasks, offs = read_plan(bufs)
+    rt, ro, _ = oracle_plan(case, p)
+    assert np.array_equal(tasks, rt)
+    assert np.array_equal(offs, ro)
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_plan_bit_exact_random_batches(seed):
+    r = np.random.Generator(np.random.PCG64(100 + seed))
+    B = int(r.integers(1, 1500))
+    lens = r.integers(0, 3000, size=B).astype(np.int32)
+    lens[r.random(B) < 0.3] = 0
+    case = Case(lens, hkv=int(r.choice([1, 2, 4, 8])), hq=8, seed=seed, rho=0.0, values=False)
+    p = plan_params(case.hkv, int(r.integers(1, 4)), int(r.integers(4, 40)), int(r.integers(1, 20000)))
+    bufs = bufs_for(case, p.split_max)
+    run_plan(case, bufs, p)
+    tasks, offs = read_plan(bufs)
+    rt, ro, _ = oracle_plan(case, p)
+    assert np.array_equal(tasks, rt) and np.array_equal(offs, ro)
+
+
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (8, 8), (16, 8), (32, 4)])
+def test_decode_ragged_matches_oracle(fused, hq, hkv):
+    case = Case(RAGGED, hq=hq, hkv=hkv, seed=2)
+    p = plan_params(hkv, 2, 16, 64)
+    bufs = bufs_for(case, 16)
+    run_plan(case, bufs, p)
+    out = run_decode(case, bufs, fused=fused)
+    ref = ref_decode(case.q, case.k, case.v, case.bt, case.lens)
+    assert_close(out, ref, f"G={hq // hkv} fused={fused}")
+    assert torch.all(out[11] == 0)  # the empty row
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+def test_sm_scale_is_applied():
+    case = Case([300, 77], seed=3)
+    bufs = bufs_for(case)
+    run_plan(case, bufs, plan_params(8, 1, 4, 16))
+    out = run_decode(case, bufs, sm_scale=0.3)
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens, 0.3), "scale 0.3")
+
+
+def test_fused_equals_two_kernel_merge_bitwise():
+    case = Case(RAGGED, seed=4)
+    bufs = bufs_for(case)
+    run_plan(case, bufs, plan_params(8, 4, 64, 700))
+    a = run_decode(case, bufs, fused=True)
+    b = run_decode(case, bufs, fused=False)
+    assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("S", [1, 3, 16, 64])
+def test_workqueue_equals_rectangular_bitwise(S):
+    case = Case(RAGGED, seed=5)
+    bufs = bufs_for(case, split_max=S, rect_splits=S)
+    run_plan(case, bufs, plan_params(8, S, S, 1))
+    wq = run_decode(case, bufs, fused=True)
+    rect = run_rect(case, bufs, S)
+    assert torch.equal(wq, rect)
+    assert_close(rect, ref_decode_rect(case.q, case.k, case.v, case.bt, case.lens, S, 32), f"rect S={S}")
+
+
+def test_physical_page_permutation_is_bitwise_invariant():
+    lens = [700, 33, 1600]
+    a = Case(lens, seed=6, rho=0.5)
+    # same logical K/V, different physical pages
+    r = np.random.Generator(np.random.PCG64(60))
+    perm = r.permutation(a.num_pages)
+    bt2 = np.where(a.bt >= 0, perm[np.maximum(a.bt, 0)], -1).astype(np.int32)
+    k2 = np.empty_like(a.k)
+    v2 = np.empty_like(a.v)
+    k2[perm] = a.k
+    v2[perm] = a.v
+    b = Case(lens, seed=6, rho=0.5)
+    b.bt, b.k, b.v = bt2, k2, v2
+    b.bt_dev, b.k_dev, b.v_dev = (torch.from_numpy(x).cuda() for x in (bt2, k2, v2))
+    outs = []
+    for c in (a, b):
+        bufs = bufs_for(c)
+        run_plan(c, bufs, plan_params(8))
+        outs.append(run_decode(c, bufs))
+    assert torch.equal(outs[0], outs[1])
+
+
+def test_one_token_context_returns_v_exactly():
+    case = Case([1, 1, 1, 1], seed=7)
+    bufs = bufs_for(case)
+    run_plan(case, bufs, plan_params(8))
+    out = run_decode(case, bufs).cpu().numpy()
+    for i in range(4):
+        v0 = case.v[case.bt[i, 0], 0]            # [Hkv, d]
+        assert np.array_equal(out[i], np.repeat(v0, 4, axis=0))
+
+
+def test_all_rows_empty_gives_zeros():
+    case = Case([0, 0, 0], seed=8)
+    for fused in (True, False):
+        bufs = bufs_for(case)
+        run_plan(case, bufs, plan_params(8))
+        assert int(bufs.num_tasks.item()) == 0
+        out = run_decode(case, bufs, fused=fused)
+        assert torch.all(out == 0)
+
+
+def test_repeated_fused_calls_are_identical():
+    case = Case([5000, 3000, 40, 9000], seed=9)
+    bufs = bufs_for(case)
+    run_plan(case, bufs, plan_params(8, 16, 64, 2048))
+    first = run_decode(case, bufs, poison_ws=False)
+    for _ in range(200):
+        again = run_decode(case, bufs, poison_ws=False)
+        assert torch.equal(first, again)
+    assert_close(first, ref_decode(case.q, case.k, case.v, case.bt, case.lens), "repeat")
+
+
+def test_sequence_longer_than_block_table_is_flagged_and_zeroed():
+    case = Case([100, 50], seed=10)
+    lens_bad = case.lens.copy()
+    lens_bad[1] = case.bt.shape[1] * 16 + 1
+    case.lens_dev = torch.from_numpy(lens_bad).cuda()
+    bufs = bufs_for(case)
+    run_plan(case, bufs, plan_params(8))
+    out = run_decode(case, bufs)
+    assert pkv.pkv_check_device_status(bufs.ws) & pkv.PKV_DEVERR_SEQ_LEN
+    assert torch.all(out[1] == 0)
+    good = ref_decode(case.q[:1], case.k, case.v, case.bt[:1], case.lens[:1])
+    assert_close(out[:1], good, "row 0")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0  # cleared by the previous read
+
+
+def test_bad_page_id_is_flagged_and_row_zeroed():
+    case = Case([100, 200], seed=11)
+    bt_bad = case.bt.copy()
+    bt_bad[0, 3] = case.num_pages + 7
+    case.bt_dev = torch.from_numpy(bt_bad).cuda()
+    for fused in (True, False):
+        bufs = bufs_for(case)
+        run_plan(case, bufs, plan_params(8))
+        out = run_decode(case, bufs, fused=fused)
+        assert pkv.pkv_check_device_status(bufs.ws) & pkv.PKV_DEVERR_PAGE_ID
+        assert torch.all(out[0] == 0)
+        assert_close(out[1:], ref_decode(case.q[1:], case.k, case.v, case.bt[1:], case.lens[1:]), "row 1")
+    # the planner's optional page check drops the row up front
+    bufs = bufs_for(case)
+    run_plan(case, bufs, plan_params(8), check_pages=True)
+    tasks, offs = read_plan(bufs)
+    assert offs[1] == 0 and np.all(tasks[:, 0] == 1)
+    assert pkv.pkv_check_device_status(bufs.ws) & pkv.PKV_DEVERR_PAGE_ID
+
+
+@pytest.mark.parametrize("name", ["tiny", "b1", "b8_bimodal", "b8_uniform", "b8_zipf", "b4_bimodal"])
+def test_benchmark_configs_full_size(name):
+    """Every output of the first decode step of each benchmark configuration, in the
+    launch configuration the benchmark times (planner + fused kernel)."""
+    case, w = Case.from_workload(name)
+    p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens)
+    bufs = bufs_for(case, w.split_max)
+    run_plan(case, bufs, p)
+    tasks, offs = read_plan(bufs)
+    rt, ro, _ = oracle_plan(case, p)
+    assert np.array_equal(tasks, rt) and np.array_equal(offs, ro)
+    out = run_decode(case, bufs)
+    ref = ref_decode(case.q, case.k, case.v, case.bt, case.lens)
+    amax, rel = assert_close(out, ref, name)
+    assert ulp_fraction(out, ref) > 0.99
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+def test_b1_last_step_and_uniform_rect():
+    case, w = Case.from_workload("b1", step=19)
+    bufs = bufs_for(case, w.split_max)
+    run_plan(case, bufs, plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks))
+    out = run_decode(case, bufs)
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), "b1 step 19")
+    case, w = Case.from_workload("b8_uniform")
+    bufs = bufs_for(case, 16, rect_splits=16)
+    run_plan(case, bufs, plan_params(w.hkv, 16, 16, 1))
+    wq = run_decode(case, bufs)
+    rect = run_rect(case, bufs, 16)
+    assert torch.equal(wq, rect)
