@@ -1,0 +1,309 @@
+#!/usr/bin/env python
+"""Decode throughput of the paged GQA decode path on one MI355X.
+
+One step is one decode step of the whole path for every active row: the planner kernel
+(compact workqueue) and the fused split-attention + last-arriver merge kernel, over a
+native paged KV cache (Hq=32, Hkv=8, d=128, fp16, page 16). Before each step, outside
+the timed region, the step's new token K/V is written into the pool, seq_lens grows by
+one, and a 1 GiB streaming read evicts the 256 MB last-level cache (MALL) so that KV is
+read from HBM as it would be with the other layers' KV in between. The eviction reads
+only, so no dirty lines are left to be written back during the timed step.
+
+Timing: HIP events on the stream the kernels run on, around each step (plan + decode)
+and around the decode kernel alone. Steps are enqueued back to back behind the cache
+eviction copy, so the events measure device time, not Python launch latency; a second,
+host-synchronized pass gives wall time per step.
+
+value = decode tokens / second = sum of active rows over the timed steps / sum of step
+times. roofline.achieved = algorithmic bytes of one decode-kernel launch / its average
+duration. cpu_baseline = the fp64 numpy oracle on the host over the same steps.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode tokens/sec per step + achieved HBM GB/s (% of MI355X peak), B1/B8"
+HBM_PEAK_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_26666_amd", "csrc", "pkv_kernels.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+KV_BYTES_PER_TOKEN = 2 * 8 * 128 * 2   # K and V, Hkv=8, d=128, fp16
+SLOT_BYTES = 2080                      # fp32 m[4], l[4], acc[4][128]
+TASK_BYTES = 20
+
+
+def kernel_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(lens, num_tasks, hq=32, d=128):
+    """Bytes one decode-kernel launch must move: K/V of every attended token, Q and out,
+    the block-table entries and lengths read, the task list, and each task's partial
+    state written once and read once by the merge."""
+    lens = np.asarray(lens, dtype=np.int64)
+    B = lens.size
+    kv = KV_BYTES_PER_TOKEN * int(lens.sum())
+    qo = 2 * B * hq * d * 2
+    meta = 4 * int(((lens + 15) // 16).sum()) + 4 * B + 4 * (B + 1) + TASK_BYTES * num_tasks
+    partial = 2 * SLOT_BYTES * num_tasks
+    return kv + qo + meta + partial, kv
+
+
+class Runner:
+    """Device state of one workload: pools, block table, lengths, buffers."""
+
+    def __init__(self, name, seed, target_tasks, steps, fused=True):
+        import torch
+
+        import paper_2606_26666_amd as pkv
+        from workloads import make_workload
+        from workloads.values import device_normal_f16, q_values
+
+        self.torch, self.pkv = torch, pkv
+        self.w = w = make_workload(name, seed=seed, steps=steps, target_tasks=target_tasks)
+        self.dev = torch.device("cuda:0")
+        shape = (w.num_pages, w.page_size, w.hkv, w.head_dim)
+        self.k = device_normal_f16(shape, seed * 4 + 1, self.dev)
+        self.v = device_normal_f16(shape, seed * 4 + 2, self.dev)
+        r = np.random.Generator(np.random.PCG64(seed + 7))
+        self.q = torch.from_numpy(q_values(w.batch, w.hq, w.head_dim, r)).to(self.dev)
+        self.bt = torch.from_numpy(w.block_table).to(self.dev)
+        self.lens = torch.from_numpy(w.lengths_at(0)).to(self.dev)
+        self.out = torch.empty((w.batch, w.hq, w.head_dim), dtype=torch.float16, device=self.dev)
+        self.bufs = pkv.DecodeBuffers(w.batch, w.hq, w.hkv, w.head_dim, w.split_max, self.dev)
+        self.params = pkv.make_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens)
+        self.fused = fused
+        self.gen = torch.Generator(device=self.dev)
+        self.gen.manual_seed(seed * 4 + 3)
+        self.bt_host = w.block_table
+
+    def host_lengths(self, step):
+        return self.w.lengths_at(step)
+
+    def prepare(self, steps):
+        """Per-step lengths and append positions, staged on the device up front so the
+        timed loop never waits on a host copy."""
+        torch, w = self.torch, self.w
+        lens = np.stack([w.lengths_at(s) for s in range(steps)])
+        pos = lens.astype(np.int64) - 1
+        pages = self.bt_host[np.arange(w.batch)[None, :], pos // w.page_size].astype(np.int64)
+        self.lens_steps = torch.from_numpy(lens).to(self.dev)
+        self.pages_steps = torch.from_numpy(pages).to(self.dev)
+        self.slots_steps = torch.from_numpy(pos % w.page_size).to(self.dev)
+        self.lens_host = lens
+
+    def append(self, step):
+        """Write step `step`'s new token K/V at the row's last position and set seq_lens
+        (all enqueued on the stream, no host synchronization)."""
+        torch, w = self.torch, self.w
+        if w.append:
+            nk = torch.randn((w.batch, w.hkv, w.head_dim), generator=self.gen, device=self.dev).half()
+            nv = torch.randn((w.batch, w.hkv, w.head_dim), generator=self.gen, device=self.dev).half()
+            self.k[self.pages_steps[step], self.slots_steps[step]] = nk
+            self.v[self.pages_steps[step], self.slots_steps[step]] = nv
+        self.lens.copy_(self.lens_steps[step])
+        return self.lens_host[step]
+
+    def plan(self):
+        b = self.bufs
+        self.pkv.pkv_plan(self.lens, None, self.w.num_pages, self.params, b.tasks, b.split_offsets, b.num_tasks,
+                          b.ws, max_pages_per_row=self.w.max_pages_per_row)
+
+    def decode(self):
+        b = self.bufs
+        self.pkv.pkv_decode(self.q, self.k, self.v, self.bt, self.lens, b.tasks, b.split_offsets, b.num_tasks,
+                            1.0, self.out, b.ws, fused=self.fused)
+
+
+def measure(runner, steps, warmup, flush_bufs):
+    torch, pkv = runner.torch, runner.pkv
+    Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    def flush():
+        if flush_bufs is not None:  # read-only: leaves the cache full of clean lines
+            pkv.pkv_stream_read(flush_bufs[0], flush_bufs[1])
+
+    runner.prepare(steps)
+    runner.append(0)
+    for _ in range(warmup):
+        flush()
+        runner.plan()
+        runner.decode()
+    torch.cuda.synchronize()
+    ev = []
+    ntasks, lens_all = [], []
+    for s in range(steps):
+        lens_all.append(runner.append(s))
+        flush()
+        e0, e1, e2 = Ev(), Ev(), Ev()
+        e0.record()
+        runner.plan()
+        e1.record()
+        runner.decode()
+        e2.record()
+        ev.append((e0, e1, e2))
+        ntasks.append(runner.bufs.num_tasks.clone())
+    torch.cuda.synchronize()
+    step_ms = [a.elapsed_time(c) for a, b, c in ev]
+    plan_ms = [a.elapsed_time(b) for a, b, c in ev]
+    dec_ms = [b.elapsed_time(c) for a, b, c in ev]
+    ntasks = [int(t.item()) for t in ntasks]
+    bits = pkv.pkv_check_device_status(runner.bufs.ws)
+    if bits:
+        raise RuntimeError(f"device error bits {bits}")
+    # serving-facing wall time: host-synchronized, includes launch overhead
+    wall = []
+    for s in range(steps):
+        flush()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        runner.plan()
+        runner.decode()
+        torch.cuda.synchronize()
+        wall.append((time.perf_counter() - t0) * 1e3)
+    return dict(step_ms=step_ms, plan_ms=plan_ms, dec_ms=dec_ms, ntasks=ntasks, lens=lens_all, wall_ms=wall)
+
+
+def summarize(runner, m):
+    w = runner.w
+    tokens = w.batch * len(m["step_ms"])
+    step_s = sum(m["step_ms"]) / 1e3
+    alg, kv = zip(*(algorithmic_bytes(l, t, w.hq, w.head_dim) for l, t in zip(m["lens"], m["ntasks"])))
+    dec_avg_s = np.mean(m["dec_ms"]) / 1e3
+    achieved = float(np.mean(alg)) / dec_avg_s / 1e9
+    return {
+        "tok_s": tokens / step_s,
+        "ms_per_step": float(np.mean(m["step_ms"])),
+        "plan_ms": float(np.mean(m["plan_ms"])),
+        "decode_ms": float(np.mean(m["dec_ms"])),
+        "wall_ms_per_step": float(np.median(m["wall_ms"])),
+        "wall_tok_s": w.batch / (float(np.median(m["wall_ms"])) / 1e3),
+        "alg_bytes_per_launch": float(np.mean(alg)),
+        "kv_bytes_per_step": float(np.mean(kv)),
+        "decode_gbs": achieved,
+        "step_gbs": float(np.mean(alg)) / (float(np.mean(m["step_ms"])) / 1e3) / 1e9,
+        "tasks_per_step": float(np.mean(m["ntasks"])),
+        "launches_per_step": 2 if runner.fused else 3,
+    }
+
+
+def read_traffic(workload):
+    """HBM bytes per decode launch from the committed rocprofv3 counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"counters_split_kernel_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(runner, steps, budget_s=20.0):
+    """The fp64 oracle on the host over the same steps' inputs (bounded to ~budget_s)."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import ref_decode
+    w = runner.w
+    k = runner.k.cpu().numpy()
+    v = runner.v.cpu().numpy()
+    q = runner.q.cpu().numpy()
+    ref_decode(q, k, v, w.block_table, w.lengths_at(0))  # first-touch warmup, untimed
+    t0 = time.perf_counter()
+    done = 0
+    for s in range(steps):
+        ref_decode(q, k, v, w.block_table, w.lengths_at(s))
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
+    return {"value": done * w.batch / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{w.name}: {done} decode steps (of {steps}) of the fp64 numpy oracle, "
+                      f"{dt:.1f} s, BLAS threads {threads}, host CPUs {len(os.sched_getaffinity(0))}"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="b1")
+    ap.add_argument("--also", default="b8_bimodal", help="comma-separated extra workloads, or 'none'")
+    ap.add_argument("--seed", type=int, default=20260623)
+    ap.add_argument("--target-tasks", type=int, default=512)
+    ap.add_argument("--two-kernel-merge", action="store_true", help="ablation: split kernel + merge kernel")
+    ap.add_argument("--no-flush", action="store_true", help="keep KV warm in the last-level cache")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one MI355X: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    import paper_2606_26666_amd as pkv
+    pkv.lib()  # fail loudly when the HIP library is missing
+
+    flush_bufs = None
+    if not args.no_flush:
+        flush_bufs = (torch.zeros(1 << 30, dtype=torch.uint8, device="cuda"),
+                      torch.zeros(1, dtype=torch.int32, device="cuda"))
+
+    steps_cfg = max(args.steps, 20 if args.workload == "b1" else 50)
+    main_run = Runner(args.workload, args.seed, args.target_tasks, steps_cfg, fused=not args.two_kernel_merge)
+    m = measure(main_run, args.steps, args.warmup, flush_bufs)
+    s = summarize(main_run, m)
+    extra = {args.workload: s}
+    for name in [x for x in args.also.split(",") if x and x != "none" and x != args.workload]:
+        r = Runner(name, args.seed, args.target_tasks, 50, fused=not args.two_kernel_merge)
+        extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
+        del r
+    traffic = read_traffic(args.workload)
+    line = {
+        "metric": METRIC,
+        "value": s["tok_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": s["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, **{k: v for k, v in main_run.w.describe().items() if k != "workload"},
+                   "kv_layout": "[num_pages,16,Hkv,d]", "accumulate": "f32",
+                   "route": "workqueue, fused merge" if not args.two_kernel_merge else "workqueue, merge kernel",
+                   "llc_flushed": not args.no_flush, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": s["decode_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": s["decode_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "split_kernel (fused)", "alg_bytes_per_launch": s["alg_bytes_per_launch"],
+                     "kernel_source_sha256": kernel_hash()},
+        "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(main_run, args.steps),
+        "extra": extra,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -155,10 +155,15 @@ int pkv_check_device_status(void* ws, hipStream_t stream, uint32_t* error_bits);
 /* Static text for a status code. */
 const char* pkv_status_string(int status);
 
-/* Streaming copy of `bytes` (a multiple of 16) from src to dst on `stream`: the
- * bandwidth probe used to calibrate HBM traffic counters and to evict the last-level
- * cache between timed steps. */
+/* Streaming copy of `bytes` (a multiple of 16) from src to dst on `stream`: a kernel of
+ * known traffic, used to calibrate HBM traffic counters. */
 int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+
+/* Streaming read of `bytes` (a multiple of 16) at src on `stream`: the read-bandwidth
+ * probe (the paper's streaming-bandwidth calibration, Sec. 3.5) and a way to evict the
+ * last-level cache with clean lines between timed steps. `sink` is a device word that
+ * is written only if the data hashes to a fixed value. */
+int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -26,6 +26,7 @@ from ._binding import (  # noqa: F401
     pkv_max_tasks,
     pkv_plan,
     pkv_stream_copy,
+    pkv_stream_read,
     pkv_workspace_init,
     pkv_workspace_size,
 )

@@ -56,6 +56,7 @@ _SIGS = {
     "pkv_check_device_status": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_uint32)]),
     "pkv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "pkv_stream_copy": (ctypes.c_int, [_P, _P, _SZ, _P]),
+    "pkv_stream_read": (ctypes.c_int, [_P, _SZ, _P, _P]),
 }
 
 
@@ -177,6 +178,14 @@ def pkv_stream_copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
         raise TypeError("pkv_stream_copy needs contiguous device tensors")
     n = min(src.numel() * src.element_size(), dst.numel() * dst.element_size())
     _check("pkv_stream_copy", lib().pkv_stream_copy(src.data_ptr(), dst.data_ptr(), n - n % 16, _stream(stream)))
+
+
+def pkv_stream_read(src: torch.Tensor, sink: torch.Tensor, stream=None):
+    if not (src.is_cuda and src.is_contiguous()):
+        raise TypeError("pkv_stream_read needs a contiguous device tensor")
+    n = src.numel() * src.element_size()
+    _check("pkv_stream_read", lib().pkv_stream_read(src.data_ptr(), n - n % 16, _dev(sink, torch.int32, "sink"),
+                                                    _stream(stream)))
 
 
 class DecodeBuffers:

@@ -196,4 +196,9 @@ int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream
   return from_hip(launch_copy(src, dst, bytes, stream));
 }
 
+int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream) {
+  if (!src || !sink || bytes % 16 != 0 || !aligned(src, 16) || !aligned(sink, 4)) return PKV_ERR_INVALID_ARG;
+  return from_hip(launch_read(src, bytes, sink, stream));
+}
+
 }  // extern "C"

@@ -59,5 +59,6 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s);
 
 }  // namespace pkv

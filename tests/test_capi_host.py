@@ -22,7 +22,7 @@ def test_exports_every_header_function():
     L = lib()
     names = pkv.header_functions()
     assert {"pkv_plan", "pkv_decode", "pkv_decode_rect", "pkv_max_tasks", "pkv_workspace_size",
-            "pkv_workspace_init", "pkv_check_device_status", "pkv_status_string", "pkv_stream_copy"} <= set(names)
+            "pkv_workspace_init", "pkv_check_device_status", "pkv_status_string", "pkv_stream_copy", "pkv_stream_read"} <= set(names)
     for n in names:
         assert hasattr(L, n), n
 
@@ -126,6 +126,8 @@ def test_copy_and_init_validation():
     L = lib()
     assert L.pkv_stream_copy(FAKE, FAKE, 15, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_stream_copy(0, FAKE, 16, None) == pkv.PKV_ERR_INVALID_ARG
+    assert L.pkv_stream_read(FAKE, 17, FAKE, None) == pkv.PKV_ERR_INVALID_ARG
+    assert L.pkv_stream_read(FAKE, 16, 0, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_workspace_init(FAKE, 100, 1, 8, None) == pkv.PKV_ERR_WORKSPACE
     assert L.pkv_workspace_init(0, 1 << 20, 1, 8, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_check_device_status(0, None, None) == pkv.PKV_ERR_INVALID_ARG
