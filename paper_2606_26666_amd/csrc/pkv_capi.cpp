@@ -137,6 +137,7 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
   if (!std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
   if (max_tasks < 1) return PKV_ERR_INVALID_ARG;
   if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, max_tasks)) return PKV_ERR_WORKSPACE;
+  if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
                            Hkv, sm_scale, out, ws);
   a.tasks = tasks;
@@ -160,6 +161,7 @@ int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
   const int32_t slots = pkv_max_tasks(B, Hkv, S);
   if (slots < 0) return PKV_ERR_INVALID_ARG;
   if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, slots)) return PKV_ERR_WORKSPACE;
+  if ((int64_t)slots * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
                            Hkv, sm_scale, out, ws);
   a.S = S;

@@ -15,7 +15,8 @@ constexpr int kMaxPlanBatch = 4096;
 constexpr size_t kWsHeaderBytes = 256;
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
-inline size_t slot_floats(int G) { return size_t(2 * G + G * kHeadDim); }
+// fp32 acc[G][d], m[G], l[G], padded to 16 bytes
+inline size_t slot_floats(int G) { return size_t(G * kHeadDim + ((2 * G + 3) / 4) * 4); }
 inline size_t counters_bytes(int B, int Hkv) { return align256(size_t(B) * size_t(Hkv) * 4); }
 inline size_t partials_offset(int B, int Hkv) { return kWsHeaderBytes + counters_bytes(B, Hkv); }
 

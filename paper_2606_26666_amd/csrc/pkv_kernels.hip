@@ -82,109 +82,217 @@ __device__ __forceinline__ void unpack8(const uint4& u, float f[8]) {
 constexpr float kNegInf = -__builtin_inff();
 
 // ---------------------------------------------------------------------------------
+// Partial-state slots (one per task): fp32 acc[G][D], then m[G] and l[G], padded to a
+// multiple of 16 bytes. m is in log2 units: scores are scaled by sm_scale*log2(e) and
+// exponentiated with exp2. l < 0 marks a split that met an invalid page.
+template <int G> constexpr int slot_floats() { return G * D + ((2 * G + 3) / 4) * 4; }
+
+// Slots are accessed through one raw buffer descriptor over the whole slot array. When
+// another workgroup merges them inside the same kernel they use agent-scope (sc1)
+// accesses, which on gfx950 are coherent across the per-XCD L2 caches, so a completed
+// store is visible on every XCD without a full L2 write-back.
+constexpr int kSc1 = 16;  // cache-policy operand of a buffer access: sc1
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t slots_rsrc(const DecodeArgs& a, int slot_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(a.partials, (short)0, a.max_tasks * slot_bytes, 0x00020000);
+}
+
+template <bool COHERENT>
+__device__ __forceinline__ float ld_state(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, COHERENT ? kSc1 : 0));
+}
+template <bool COHERENT>
+__device__ __forceinline__ v4f ld_state4(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, COHERENT ? kSc1 : 0));
+}
+template <bool COHERENT>
+__device__ __forceinline__ void st_state(__amdgpu_buffer_rsrc_t r, int off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), r, off, 0, COHERENT ? kSc1 : 0);
+}
+template <bool COHERENT>
+__device__ __forceinline__ void st_state4(__amdgpu_buffer_rsrc_t r, int off, v4f v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, v), r, off, 0, COHERENT ? kSc1 : 0);
+}
+
+// ---------------------------------------------------------------------------------
 // Merge of split states (Sec. 3.3): M = max m_s, L = sum 2^(m_s-M) l_s,
-// A = sum 2^(m_s-M) a_s, O = A / L, summed in split order. States hold m in log2 units.
-// l_s < 0 marks a split that met an invalid page; such a (row, KV head) is zeroed.
-// Every merge in the library goes through merge_group, so all routes round identically.
-constexpr int kMergeChunk = 64;  // split states staged in LDS at a time
-
-// Partial states that another workgroup merges inside the same kernel are written and
-// read with agent-scope (sc1) accesses: on gfx950 these bypass the per-XCD L2 caches,
-// so completed stores are visible to every XCD without a full L2 write-back.
-template <bool COHERENT>
-__device__ __forceinline__ float load_state(const float* p) {
-  if (COHERENT) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return *p;
-}
-
-template <bool COHERENT>
-__device__ __forceinline__ void store_state(float* p, float v) {
-  if (COHERENT) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  else *p = v;
-}
+// A = sum 2^(m_s-M) a_s, O = A / L. The sums follow a fixed tree: splits in order
+// within runs of kMergeRun, run sums added in order, so the result does not depend on
+// the thread count. Every merge in the library goes through merge_group, so all routes
+// round identically. A (row, KV head) with a marked split (l < 0) is zeroed.
+//
+// Latency: for up to kMergeBlock splits, a thread's acc loads (one run of one float4
+// column) and the m/l loads are in flight together, so the merge costs about one
+// memory round trip.
+constexpr int kMergeBlock = 64;  // split states staged in LDS at a time
+constexpr int kMergeRun = 32;    // splits per run
+constexpr int kRunsPerBlock = kMergeBlock / kMergeRun;
+constexpr int kMaxMergeWaves = 16;
 
 template <int G>
-constexpr int merge_lds_floats() { return 2 * kMergeChunk * G; }
+constexpr int merge_lds_floats() {
+  return 2 * kMergeBlock * G + kRunsPerBlock * G * D + kRunsPerBlock * G + 2 * kMaxMergeWaves * G + 3 * G;
+}
 
 // The nsplit states at slots slot0 + s*stride (s < nsplit) of one (row, KV head) into
 // out_grp[G][D] (fp16). All NT threads of the workgroup take part.
 template <int G, int NT, bool COHERENT>
-__device__ __forceinline__ void merge_group(const float* __restrict__ partials, int slot0, int stride, int nsplit,
+__device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0, int stride, int nsplit,
                                             uint16_t* __restrict__ out_grp, float* lds) {
-  constexpr int SF = 2 * G + G * D;
-  constexpr int EPT = (G * D + NT - 1) / NT;  // output elements per thread
-  float* lm = lds;                       // [chunk][G]
-  float* ll = lds + kMergeChunk * G;     // [chunk][G]
+  static_assert(NT % 64 == 0 && NT / 64 <= kMaxMergeWaves && 64 % G == 0, "merge shape");
+  constexpr int SB = slot_floats<G>() * 4;            // slot bytes
+  constexpr int E4 = G * D / 4;                       // float4 columns of the output
+  constexpr int EPT = (G * D + NT - 1) / NT;          // output elements per thread
+  constexpr int KPT = (kMergeBlock * G + NT - 1) / NT;  // (split, head) states per thread
+  float* lw = lds;                                    // [block][G] weights 2^(m-M)
+  float* ll = lw + kMergeBlock * G;                   // [block][G] l
+  float* part = ll + kMergeBlock * G;                 // [run][G*D] run sums of acc
+  float* partL = part + kRunsPerBlock * G * D;        // [run][G] run sums of l
+  float* redM = partL + kRunsPerBlock * G;            // [wave][G]
+  float* redB = redM + kMaxMergeWaves * G;            // [wave][G]
+  float* sM = redB + kMaxMergeWaves * G;              // [G] max
+  float* sBad = sM + G;                               // [G]
+  float* sL = sBad + G;                               // [G] running L
   const int tid = threadIdx.x;
-  auto stage = [&](int s0, int cnt) {
-    for (int e = tid; e < cnt * G; e += NT) {
-      const float* st = partials + (size_t)(slot0 + (s0 + e / G) * stride) * SF;
-      lm[e] = load_state<COHERENT>(st + e % G);
-      ll[e] = load_state<COHERENT>(st + G + e % G);
-    }
-  };
-  float M[EPT], L[EPT], A[EPT];
-  bool bad[EPT];
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int myh = tid % G;  // the head of every (split, head) state this thread loads
+  auto soff = [&](int s) { return (slot0 + s * stride) * SB; };
+
+  float mv[KPT], lv[KPT];
+  auto load_ml = [&](int s0, int cnt) {
 #pragma unroll
-  for (int q = 0; q < EPT; ++q) {
-    M[q] = kNegInf;
-    L[q] = 0.0f;
-    A[q] = 0.0f;
-    bad[q] = false;
-  }
-  // pass 1: per-head maximum over all splits
-  for (int s0 = 0; s0 < nsplit; s0 += kMergeChunk) {
-    const int cnt = min(kMergeChunk, nsplit - s0);
-    __syncthreads();
-    stage(s0, cnt);
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < EPT; ++q) {
-      const int h = min((tid + q * NT) / D, G - 1);
-      for (int s = 0; s < cnt; ++s) {
-        M[q] = fmaxf(M[q], lm[s * G + h]);
-        bad[q] |= ll[s * G + h] < 0.0f;
+    for (int k = 0; k < KPT; ++k) {
+      const int e = tid + k * NT;
+      if (e < cnt * G) {
+        mv[k] = ld_state<COHERENT>(pr, soff(s0 + e / G) + (G * D + myh) * 4);
+        lv[k] = ld_state<COHERENT>(pr, soff(s0 + e / G) + (G * D + G + myh) * 4);
+      } else {
+        mv[k] = kNegInf;
+        lv[k] = 0.0f;
       }
     }
-  }
-  // pass 2: weighted sums in split order; acc loads issued in batches of 8
-  for (int s0 = 0; s0 < nsplit; s0 += kMergeChunk) {
-    const int cnt = min(kMergeChunk, nsplit - s0);
-    if (s0 > 0) {
-      __syncthreads();
-      stage(s0, cnt);
-      __syncthreads();
+  };
+  // max and marker over this thread's states, then over lanes of the same head, then
+  // over waves; folded into sM / sBad (exact: max does not depend on the order)
+  auto reduce_max = [&]() {
+    float mx = kNegInf, bd = 0.0f;
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      mx = fmaxf(mx, mv[k]);
+      bd = fmaxf(bd, lv[k] < 0.0f ? 1.0f : 0.0f);
     }
+#pragma unroll
+    for (int sh = G; sh < 64; sh <<= 1) {
+      mx = fmaxf(mx, __shfl_xor(mx, sh));
+      bd = fmaxf(bd, __shfl_xor(bd, sh));
+    }
+    if (lane < G) {
+      redM[wave * G + lane] = mx;
+      redB[wave * G + lane] = bd;
+    }
+    __syncthreads();
+    if (tid < G) {
+      float m2 = sM[tid], b2 = sBad[tid];
+      for (int w = 0; w < NT / 64; ++w) {
+        m2 = fmaxf(m2, redM[w * G + tid]);
+        b2 = fmaxf(b2, redB[w * G + tid]);
+      }
+      sM[tid] = m2;
+      sBad[tid] = b2;
+    }
+    __syncthreads();
+  };
+
+  if (tid < G) {
+    sM[tid] = kNegInf;
+    sBad[tid] = 0.0f;
+    sL[tid] = 0.0f;
+  }
+  const bool one_block = nsplit <= kMergeBlock;
+  if (!one_block) {  // pass 1: maximum over every block first
+    for (int s0 = 0; s0 < nsplit; s0 += kMergeBlock) {
+      load_ml(s0, min(kMergeBlock, nsplit - s0));
+      reduce_max();
+    }
+  }
+  float A[EPT];
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) A[q] = 0.0f;
+  v4f v[kMergeRun];
+  for (int s0 = 0; s0 < nsplit; s0 += kMergeBlock) {
+    const int cnt = min(kMergeBlock, nsplit - s0);
+    const int nrun = (cnt + kMergeRun - 1) / kMergeRun;
+    const int nitems = E4 * nrun;
+    auto issue_item = [&](int it) {
+      const int e4 = it % E4;
+      const int sb = (it / E4) * kMergeRun;
+      const int n = min(kMergeRun, cnt - sb);
+#pragma unroll
+      for (int u = 0; u < kMergeRun; ++u)
+        if (u < n) v[u] = ld_state4<COHERENT>(pr, soff(s0 + sb + u) + e4 * 16);
+    };
+    auto finish_item = [&](int it) {
+      const int e4 = it % E4;
+      const int run = it / E4;
+      const int sb = run * kMergeRun;
+      const int n = min(kMergeRun, cnt - sb);
+      const int h = (e4 * 4) / D;
+      v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      float lacc = 0.0f;
+      const bool first_col = (e4 * 4) % D == 0;
+#pragma unroll
+      for (int u = 0; u < kMergeRun; ++u) {
+        if (u < n) {
+          const float w = lw[(sb + u) * G + h];
+          acc.x = __builtin_fmaf(w, v[u].x, acc.x);
+          acc.y = __builtin_fmaf(w, v[u].y, acc.y);
+          acc.z = __builtin_fmaf(w, v[u].z, acc.z);
+          acc.w = __builtin_fmaf(w, v[u].w, acc.w);
+          if (first_col) lacc = __builtin_fmaf(w, ll[(sb + u) * G + h], lacc);
+        }
+      }
+      *reinterpret_cast<v4f*>(part + run * G * D + e4 * 4) = acc;
+      if (first_col) partL[run * G + h] = lacc;
+    };
+    __syncthreads();  // the previous block's LDS is consumed
+    if (tid < nitems) issue_item(tid);  // in flight while m and l arrive
+    load_ml(s0, cnt);
+    if (one_block) reduce_max();
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const int e = tid + k * NT;
+      if (e < cnt * G) {
+        const float M = sM[myh];
+        lw[e] = ex2(mv[k] - (M == kNegInf ? 0.0f : M));
+        ll[e] = lv[k];
+      }
+    }
+    __syncthreads();
+    if (tid < nitems) finish_item(tid);
+    for (int it = tid + NT; it < nitems; it += NT) {
+      issue_item(it);
+      finish_item(it);
+    }
+    __syncthreads();
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
       const int e = tid + q * NT;
-      if (e >= G * D) break;
-      const int h = e / D;
-      const float* ap = partials + (size_t)(slot0 + s0 * stride) * SF + 2 * G + e;
-      int s = 0;
-      for (; s + 8 <= cnt; s += 8) {
-        float v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = load_state<COHERENT>(ap + (size_t)(s + u) * stride * SF);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const float c = ex2(lm[(s + u) * G + h] - M[q]);
-          L[q] = __builtin_fmaf(c, ll[(s + u) * G + h], L[q]);
-          A[q] = __builtin_fmaf(c, v[u], A[q]);
-        }
-      }
-      for (; s < cnt; ++s) {
-        const float c = ex2(lm[s * G + h] - M[q]);
-        L[q] = __builtin_fmaf(c, ll[s * G + h], L[q]);
-        A[q] = __builtin_fmaf(c, load_state<COHERENT>(ap + (size_t)s * stride * SF), A[q]);
-      }
+      if (e < G * D)
+        for (int run = 0; run < nrun; ++run) A[q] += part[run * G * D + e];
     }
+    if (tid < G)
+      for (int run = 0; run < nrun; ++run) sL[tid] += partL[run * G + tid];
   }
+  __syncthreads();
 #pragma unroll
   for (int q = 0; q < EPT; ++q) {
     const int e = tid + q * NT;
     if (e >= G * D) break;
-    const float o = (M[q] == kNegInf || bad[q]) ? 0.0f : A[q] / L[q];
+    const int h = e / D;
+    const float o = (sM[h] == kNegInf || sBad[h] != 0.0f) ? 0.0f : A[q] / sL[h];
     out_grp[e] = f32_to_f16_bits(o);
   }
 }
@@ -194,7 +302,6 @@ __device__ __forceinline__ void merge_group(const float* __restrict__ partials, 
 template <int G, int W, bool COHERENT>
 __device__ __forceinline__ void run_task(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
                                          float* lds) {
-  constexpr int SF = 2 * G + G * D;
   float* lds_m = lds;                // [W][G]
   float* lds_l = lds + W * G;        // [W][G]
   float* lds_acc = lds + 2 * W * G;  // [W][G][D]
@@ -373,34 +480,40 @@ __device__ __forceinline__ void run_task(const DecodeArgs& a, int row, int g, in
   for (int w = 0; w < W; ++w) any_bad |= lds_bad[w] != 0;
   if (any_bad && threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
 
-  float* st = a.partials + (size_t)slot * SF;
-  for (int e = threadIdx.x; e < G * D; e += W * 64) {
-    const int h = e / D;
-    const int dcol = e % D;
+  constexpr int SB = slot_floats<G>() * 4;
+  const __amdgpu_buffer_rsrc_t pr = slots_rsrc(a, SB);
+  for (int e4 = threadIdx.x; e4 < G * D / 4; e4 += W * 64) {
+    const int h = (e4 * 4) / D;
     float M = kNegInf;
 #pragma unroll
     for (int w = 0; w < W; ++w) M = fmaxf(M, lds_m[w * G + h]);
     const float Mref = (M == kNegInf) ? 0.0f : M;
-    float L = 0.0f, A = 0.0f;
+    float L = 0.0f;
+    v4f A = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int w = 0; w < W; ++w) {
       const float cf = ex2(lds_m[w * G + h] - Mref);
+      const v4f x = *reinterpret_cast<const v4f*>(lds_acc + (size_t)w * G * D + e4 * 4);
       L = __builtin_fmaf(cf, lds_l[w * G + h], L);
-      A = __builtin_fmaf(cf, lds_acc[((size_t)w * G + h) * D + dcol], A);
+      A.x = __builtin_fmaf(cf, x.x, A.x);
+      A.y = __builtin_fmaf(cf, x.y, A.y);
+      A.z = __builtin_fmaf(cf, x.z, A.z);
+      A.w = __builtin_fmaf(cf, x.w, A.w);
     }
-    store_state<COHERENT>(st + 2 * G + h * D + dcol, A);
-    if (dcol == 0) {
-      store_state<COHERENT>(st + h, M);
-      store_state<COHERENT>(st + G + h, any_bad ? -1.0f : L);
+    st_state4<COHERENT>(pr, slot * SB + e4 * 16, A);
+    if ((e4 * 4) % D == 0) {
+      st_state<COHERENT>(pr, slot * SB + (G * D + h) * 4, M);
+      st_state<COHERENT>(pr, slot * SB + (G * D + G + h) * 4, any_bad ? -1.0f : L);
     }
   }
 }
 
 template <int G>
 __device__ __forceinline__ void write_neutral(const DecodeArgs& a, int slot) {
-  constexpr int SF = 2 * G + G * D;
-  float* st = a.partials + (size_t)slot * SF;
-  for (int e = threadIdx.x; e < SF; e += blockDim.x) st[e] = (e < G) ? kNegInf : 0.0f;
+  constexpr int SF = slot_floats<G>();
+  const __amdgpu_buffer_rsrc_t pr = slots_rsrc(a, SF * 4);
+  for (int e = threadIdx.x; e < SF; e += blockDim.x)
+    st_state<false>(pr, (slot * SF + e) * 4, (e >= G * D && e < G * D + G) ? kNegInf : 0.0f);
 }
 
 template <int G>
@@ -458,7 +571,7 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       }
       __syncthreads();
       if (lds_last) {
-        merge_group<G, W * 64, true>(a.partials, off * a.Hkv + g, a.Hkv, nsplit,
+        merge_group<G, W * 64, true>(slots_rsrc(a, slot_floats<G>() * 4), off * a.Hkv + g, a.Hkv, nsplit,
                                a.out + ((size_t)row * a.Hq + (size_t)g * G) * D, lds_merge);
         if (threadIdx.x == 0) a.counters[row * a.Hkv + g] = 0;
       }
@@ -518,7 +631,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
       nsplit = 0;
     }
   }
-  merge_group<G, kMergeThreads, false>(a.partials, uniform(slot0), a.Hkv, uniform(nsplit),
+  merge_group<G, kMergeThreads, false>(slots_rsrc(a, slot_floats<G>() * 4), uniform(slot0), a.Hkv, uniform(nsplit),
                                 a.out + ((size_t)row * a.Hq + (size_t)g * G) * D, lds);
 }
 

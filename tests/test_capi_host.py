@@ -35,7 +35,7 @@ def test_sizes():
     # header 256 + counters (8 -> 256) + 512 slots of fp32 {m[4], l[4], acc[4][128]} = 2080 B
     assert pkv.pkv_workspace_size(1, 32, 8, 128, 512) == 256 + 256 + 512 * 2080
     assert pkv.pkv_workspace_size(8, 32, 8, 128, 10) == 256 + 256 + 10 * 2080
-    assert pkv.pkv_workspace_size(1, 8, 8, 128, 1) == 512 + 4 * (2 + 128)
+    assert pkv.pkv_workspace_size(1, 8, 8, 128, 1) == 512 + 4 * (128 + 4)    # G = 1: padded to 16 B
     assert pkv.pkv_workspace_size(1, 32, 8, 64, 1) == 0      # d != 128
     assert pkv.pkv_workspace_size(1, 30, 8, 128, 1) == 0     # Hq % Hkv
     assert pkv.pkv_workspace_size(1, 64, 4, 128, 1) == 0     # G = 16 has no kernel
