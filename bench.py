@@ -15,8 +15,11 @@ eviction copy, so the events measure device time, not Python launch latency; a s
 host-synchronized pass gives wall time per step.
 
 value = decode tokens / second = sum of active rows over the timed steps / sum of step
-times. roofline.achieved = algorithmic bytes of one decode-kernel launch / its average
-duration. cpu_baseline = the fp64 numpy oracle on the host over the same steps.
+times (event intervals around plan + decode, marker latency included). roofline.achieved
+= algorithmic bytes of one decode-kernel launch / its average duration (event interval
+around the launch less the median empty-interval latency measured in the same run; it
+agrees with rocprofv3's kernel duration). cpu_baseline = the fp64 numpy oracle on the
+host over the same steps.
 """
 from __future__ import annotations
 
@@ -61,7 +64,7 @@ def algorithmic_bytes(lens, num_tasks, hq=32, d=128):
 class Runner:
     """Device state of one workload: pools, block table, lengths, buffers."""
 
-    def __init__(self, name, seed, target_tasks, steps, fused=True):
+    def __init__(self, name, seed, target_tasks, steps, route="plan+fused", policy=0):
         import torch
 
         import paper_2606_26666_amd as pkv
@@ -80,8 +83,11 @@ class Runner:
         self.lens = torch.from_numpy(w.lengths_at(0)).to(self.dev)
         self.out = torch.empty((w.batch, w.hq, w.head_dim), dtype=torch.float16, device=self.dev)
         self.bufs = pkv.DecodeBuffers(w.batch, w.hq, w.hkv, w.head_dim, w.split_max, self.dev)
-        self.params = pkv.make_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens)
-        self.fused = fused
+        self.params = pkv.make_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens,
+                                      policy=policy)
+        self.policy = policy
+        self.route = route
+        self.fused = route != "two-kernel"
         self.gen = torch.Generator(device=self.dev)
         self.gen.manual_seed(seed * 4 + 3)
         self.bt_host = w.block_table
@@ -114,12 +120,18 @@ class Runner:
         return self.lens_host[step]
 
     def plan(self):
+        if self.route == "one-launch":
+            return  # the decode launch plans
         b = self.bufs
         self.pkv.pkv_plan(self.lens, None, self.w.num_pages, self.params, b.tasks, b.split_offsets, b.num_tasks,
                           b.ws, max_pages_per_row=self.w.max_pages_per_row)
 
     def decode(self):
         b = self.bufs
+        if self.route == "one-launch":
+            self.pkv.pkv_plan_decode(self.q, self.k, self.v, self.bt, self.lens, self.params, b.tasks,
+                                     b.split_offsets, b.num_tasks, 1.0, self.out, b.ws)
+            return
         self.pkv.pkv_decode(self.q, self.k, self.v, self.bt, self.lens, b.tasks, b.split_offsets, b.num_tasks,
                             1.0, self.out, b.ws, fused=self.fused)
 
@@ -144,6 +156,24 @@ def measure(runner, steps, warmup, flush_bufs):
     for s in range(steps):
         lens_all.append(runner.append(s))
         flush()
+        e0, e2 = Ev(), Ev()
+        e0.record()
+        runner.plan()
+        runner.decode()
+        e2.record()
+        ev.append((e0, e2))
+        ntasks.append(runner.bufs.num_tasks.clone())
+    torch.cuda.synchronize()
+    step_ms = [a.elapsed_time(c) for a, c in ev]
+    ntasks = [int(t.item()) for t in ntasks]
+    bits = pkv.pkv_check_device_status(runner.bufs.ws)
+    if bits:
+        raise RuntimeError(f"device error bits {bits}")
+    # per-kernel breakdown on the last step's inputs: events around each launch alone
+    # (kept out of the step timing above, since every event adds its own marker latency)
+    ev = []
+    for s in range(steps):
+        flush()
         e0, e1, e2 = Ev(), Ev(), Ev()
         e0.record()
         runner.plan()
@@ -151,15 +181,18 @@ def measure(runner, steps, warmup, flush_bufs):
         runner.decode()
         e2.record()
         ev.append((e0, e1, e2))
-        ntasks.append(runner.bufs.num_tasks.clone())
     torch.cuda.synchronize()
-    step_ms = [a.elapsed_time(c) for a, b, c in ev]
     plan_ms = [a.elapsed_time(b) for a, b, c in ev]
     dec_ms = [b.elapsed_time(c) for a, b, c in ev]
-    ntasks = [int(t.item()) for t in ntasks]
-    bits = pkv.pkv_check_device_status(runner.bufs.ws)
-    if bits:
-        raise RuntimeError(f"device error bits {bits}")
+    # marker latency alone: two events with nothing between them
+    ev = []
+    for s in range(steps):
+        e0, e1 = Ev(), Ev()
+        e0.record()
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    marker_ms = [a.elapsed_time(b) for a, b in ev]
     # serving-facing wall time: host-synchronized, includes launch overhead
     wall = []
     for s in range(steps):
@@ -170,7 +203,8 @@ def measure(runner, steps, warmup, flush_bufs):
         runner.decode()
         torch.cuda.synchronize()
         wall.append((time.perf_counter() - t0) * 1e3)
-    return dict(step_ms=step_ms, plan_ms=plan_ms, dec_ms=dec_ms, ntasks=ntasks, lens=lens_all, wall_ms=wall)
+    return dict(step_ms=step_ms, plan_ms=plan_ms, dec_ms=dec_ms, ntasks=ntasks, lens=lens_all, wall_ms=wall,
+                marker_ms=marker_ms)
 
 
 def summarize(runner, m):
@@ -178,21 +212,27 @@ def summarize(runner, m):
     tokens = w.batch * len(m["step_ms"])
     step_s = sum(m["step_ms"]) / 1e3
     alg, kv = zip(*(algorithmic_bytes(l, t, w.hq, w.head_dim) for l, t in zip(m["lens"], m["ntasks"])))
-    dec_avg_s = np.mean(m["dec_ms"]) / 1e3
-    achieved = float(np.mean(alg)) / dec_avg_s / 1e9
+    marker = float(np.median(m["marker_ms"]))
+    # decode-kernel duration: events around the launch, less the latency of an empty
+    # event interval (the event markers' own cost, measured in the same run)
+    dec_ms = float(np.mean(m["dec_ms"])) - marker
+    achieved = float(alg[-1]) / (dec_ms / 1e3) / 1e9  # the breakdown pass ran the last step's inputs
     return {
         "tok_s": tokens / step_s,
         "ms_per_step": float(np.mean(m["step_ms"])),
         "plan_ms": float(np.mean(m["plan_ms"])),
-        "decode_ms": float(np.mean(m["dec_ms"])),
+        "decode_event_ms": float(np.mean(m["dec_ms"])),
+        "event_marker_ms": marker,
+        "decode_ms": dec_ms,
         "wall_ms_per_step": float(np.median(m["wall_ms"])),
         "wall_tok_s": w.batch / (float(np.median(m["wall_ms"])) / 1e3),
         "alg_bytes_per_launch": float(np.mean(alg)),
+        "alg_bytes_last_step": float(alg[-1]),
         "kv_bytes_per_step": float(np.mean(kv)),
         "decode_gbs": achieved,
         "step_gbs": float(np.mean(alg)) / (float(np.mean(m["step_ms"])) / 1e3) / 1e9,
         "tasks_per_step": float(np.mean(m["ntasks"])),
-        "launches_per_step": 2 if runner.fused else 3,
+        "launches_per_step": {"one-launch": 1, "plan+fused": 2, "two-kernel": 3}[runner.route],
     }
 
 
@@ -248,7 +288,10 @@ def main():
     ap.add_argument("--also", default="b8_bimodal", help="comma-separated extra workloads, or 'none'")
     ap.add_argument("--seed", type=int, default=20260623)
     ap.add_argument("--target-tasks", type=int, default=512)
-    ap.add_argument("--two-kernel-merge", action="store_true", help="ablation: split kernel + merge kernel")
+    ap.add_argument("--policy", type=int, default=0, help="split policy: 0 batch split count, 1 tile quota")
+    ap.add_argument("--route", default="plan+fused", choices=["plan+fused", "one-launch", "two-kernel"],
+                    help="plan+fused: planner kernel + fused split/merge kernel (2 launches); one-launch: "
+                         "planner inside the decode launch; two-kernel: planner, split kernel, merge kernel")
     ap.add_argument("--no-flush", action="store_true", help="keep KV warm in the last-level cache")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -263,18 +306,25 @@ def main():
     import paper_2606_26666_amd as pkv
     pkv.lib()  # fail loudly when the HIP library is missing
 
+    # a copy of known size (64 MiB read + 64 MiB written), so that rocprofv3 FETCH_SIZE and
+    # WRITE_SIZE of this run can be scaled to bytes
+    cal = torch.zeros(2 << 26, dtype=torch.uint8, device="cuda")
+    pkv.pkv_stream_copy(cal[: 1 << 26], cal[1 << 26:])
+    torch.cuda.synchronize()
+    del cal
     flush_bufs = None
     if not args.no_flush:
         flush_bufs = (torch.zeros(1 << 30, dtype=torch.uint8, device="cuda"),
                       torch.zeros(1, dtype=torch.int32, device="cuda"))
 
     steps_cfg = max(args.steps, 20 if args.workload == "b1" else 50)
-    main_run = Runner(args.workload, args.seed, args.target_tasks, steps_cfg, fused=not args.two_kernel_merge)
+    main_run = Runner(args.workload, args.seed, args.target_tasks, steps_cfg, route=args.route,
+                      policy=args.policy)
     m = measure(main_run, args.steps, args.warmup, flush_bufs)
     s = summarize(main_run, m)
     extra = {args.workload: s}
     for name in [x for x in args.also.split(",") if x and x != "none" and x != args.workload]:
-        r = Runner(name, args.seed, args.target_tasks, 50, fused=not args.two_kernel_merge)
+        r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
         del r
     traffic = read_traffic(args.workload)
@@ -293,11 +343,13 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, **{k: v for k, v in main_run.w.describe().items() if k != "workload"},
                    "kv_layout": "[num_pages,16,Hkv,d]", "accumulate": "f32",
-                   "route": "workqueue, fused merge" if not args.two_kernel_merge else "workqueue, merge kernel",
+                   "route": args.route,
+                   "split_policy": ["batch split count", "tile quota"][args.policy],
                    "llc_flushed": not args.no_flush, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": s["decode_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": s["decode_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "split_kernel (fused)", "alg_bytes_per_launch": s["alg_bytes_per_launch"],
+                     "kernel": "split_kernel" + (" (planner inside)" if args.route == "one-launch" else ""),
+                     "alg_bytes_per_launch": s["alg_bytes_last_step"],
                      "kernel_source_sha256": kernel_hash()},
         "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(main_run, args.steps),
         "extra": extra,

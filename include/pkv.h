@@ -52,6 +52,7 @@ extern "C" {
 #define PKV_DEVERR_TASK 4u    /* a task outside the batch or its row's block table: skipped;
                                  outputs are unspecified unless the task list came from
                                  pkv_plan for the same seq_lens */
+#define PKV_DEVERR_PLAN_WAIT 8u /* pkv_plan_decode: a workgroup gave up waiting for the plan */
 
 /* pkv_decode flags. */
 #define PKV_FUSED_MERGE 1 /* merge in the split kernel by the last-arriving split (Sec. 3.4) */
@@ -62,15 +63,29 @@ typedef struct {
   int32_t row, kvh, split, t_begin, t_end;
 } pkv_task;
 
+/* Split policies (pkv_plan_params.policy). tiles_i = ceil(seq_len_i / tile_tokens).
+ *   PKV_SPLIT_BATCH  one split count for the step, from the active batch size
+ *                    (Sec. 3.5): S = clamp(ceil(target_tasks / max(1, B_active * Hkv)),
+ *                    split_min, split_max), B_active = rows with seq_len > 0;
+ *                    nsplit_i = min(S, tiles_i)
+ *   PKV_SPLIT_QUOTA  per-row split counts from the step's total work, so that every
+ *                    task covers about the same number of tiles (the per-row split
+ *                    count the paper names as future work, Sec. 5):
+ *                    Q = max(1, ceil(sum tiles_i / max(1, floor(target_tasks / Hkv)))),
+ *                    capped at max(1, ceil(max tiles_i / split_min));
+ *                    nsplit_i = min(split_max, ceil(tiles_i / Q)) */
+#define PKV_SPLIT_BATCH 0
+#define PKV_SPLIT_QUOTA 1
+
 /* Planner parameters (host struct).
  *   page_size    tokens per KV page; must be 16
  *   tile_tokens  split granularity in tokens (the paper's 32-token tile, Sec. 3.2);
  *                a positive multiple of page_size
  *   num_kv_heads Hkv
- *   split_min, split_max  bounds on the split count S, 1 <= split_min <= split_max
- *   target_tasks S = clamp(ceil(target_tasks / max(1, B_active * Hkv)), split_min,
- *                split_max), B_active = rows with seq_len > 0 (Sec. 3.5: the workqueue
- *                split count follows the active batch size); target_tasks >= 1 */
+ *   split_min, split_max  split-count bounds, 1 <= split_min <= split_max
+ *   target_tasks desired task count, >= 1 (see the policies above)
+ *   policy       PKV_SPLIT_BATCH or PKV_SPLIT_QUOTA
+ * Split s of row i owns tiles [floor(s*tiles_i/nsplit_i), floor((s+1)*tiles_i/nsplit_i)). */
 typedef struct {
   int32_t page_size;
   int32_t tile_tokens;
@@ -78,6 +93,7 @@ typedef struct {
   int32_t split_min;
   int32_t split_max;
   int32_t target_tasks;
+  int32_t policy;
 } pkv_plan_params;
 
 /* Upper bound on the task count of any plan: B * Hkv * split_max. Returns -1 on a
@@ -85,9 +101,12 @@ typedef struct {
 int32_t pkv_max_tasks(int32_t B, int32_t Hkv, int32_t split_max);
 
 /* Bytes of workspace for batches of up to B rows and up to max_tasks partial-state
- * slots: a 256-byte header (error word), B*Hkv completion counters, and max_tasks
- * slots of fp32 {m[G], l[G], acc[G][d]} (2080 bytes at G=4, d=128). Returns 0 on a
- * bad argument. The rectangular route needs max_tasks >= B * Hkv * S. */
+ * slots: a 256-byte header (error word, plan-ready flag), B*Hkv completion counters,
+ * and max_tasks
+ * slots of fp32 {acc[G][d], m[G], l[G]} padded to 16 bytes (2080 bytes at G=4,
+ * d=128). Returns 0 on a bad argument. The rectangular route needs
+ * max_tasks >= B * Hkv * S. One workspace serves calls with one B: pkv_plan and
+ * pkv_decode of a step must pass the same B. */
 size_t pkv_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_tasks);
 
 /* Zero the workspace header and completion counters (enqueued on `stream`). Call once
@@ -104,8 +123,7 @@ int pkv_workspace_init(void* ws, size_t ws_bytes, int32_t B, int32_t Hkv, hipStr
  *   tasks         device pkv_task [max_tasks]; entries [0, *num_tasks) are written in
  *                 (row, split, kvh) order, kvh fastest; task k's partial state lives in
  *                 slot k = (split_offsets[row] + split) * Hkv + kvh
- *   split_offsets device int32 [B+1]: split_offsets[i+1] - split_offsets[i] = splits of
- *                 row i = min(S, ceil(seq_len_i / tile_tokens))
+ *   split_offsets device int32 [B+1]: split_offsets[i+1] - split_offsets[i] = nsplit_i
  *   num_tasks     device int32 [1]
  *   ws            workspace of at least pkv_workspace_size(B, ., Hkv, ., 0) bytes; the
  *                 plan zeroes the completion counters
@@ -135,6 +153,19 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
                const pkv_task* tasks, const int32_t* split_offsets, const int32_t* num_tasks,
                int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out, void* ws,
                size_t ws_bytes, hipStream_t stream);
+
+/* pkv_plan followed by pkv_decode with PKV_FUSED_MERGE, in one kernel launch: the
+ * launch's first workgroup builds the task list (written to tasks, split_offsets and
+ * num_tasks exactly as pkv_plan writes them) and the other workgroups start on it once
+ * it is published. Arguments as for pkv_plan and pkv_decode; the block table is
+ * checked by the decode (not by the planner), B <= 1024, params->num_kv_heads == Hkv.
+ * Outputs are bit-identical to the two-call sequence. */
+int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                    int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                    const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                    const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+                    int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Rectangular split grid (Sec. 3.4): B * Hkv * S split workgroups, then a merge over
  * all S columns (two kernels, no planner). Column s of row i owns the same balanced

@@ -23,4 +23,6 @@ from .plan import (  # noqa: F401
     choose_split_count,
     ref_plan,
     row_split_bounds,
+    row_split_counts,
+    tile_quota,
 )

@@ -9,10 +9,16 @@ tokens (Sec. 3.2), and the workqueue's split count depends on the active batch s
 and the row's tile count (Sec. 3.5). It leaves the split-count formula and the split
 boundaries open; the readings taken here are:
 
-  S         = clamp(ceil(target_tasks / max(1, B_act * Hkv)), split_min, split_max),
-              B_act = number of rows with N_i > 0
   tiles_i   = ceil(N_i / T)
-  nsplit_i  = min(S, tiles_i)                      (0 for an empty row)
+  policy 0 (batch split count, the default):
+    S         = clamp(ceil(target_tasks / max(1, B_act * Hkv)), split_min, split_max),
+                B_act = number of rows with N_i > 0
+    nsplit_i  = min(S, tiles_i)                    (0 for an empty row)
+  policy 1 (tile quota: per-row split counts from the batch's total work, so that
+            every task covers about the same number of tiles):
+    Q         = max(1, ceil(sum_i tiles_i / max(1, floor(target_tasks / Hkv)))),
+                then Q = min(Q, max(1, ceil(max_i tiles_i / split_min)))
+    nsplit_i  = min(split_max, ceil(tiles_i / Q))  (0 for an empty row)
   split s of row i owns tiles [b_s, b_{s+1}),  b_s = floor(s * tiles_i / nsplit_i)
   task      = (i, g, s, b_s*T, min(b_{s+1}*T, N_i)),  for s < nsplit_i, g < Hkv
   order     = lexicographic in (row, split, kv head), kv head fastest; the task's index
@@ -34,6 +40,7 @@ class PlanParams:
     split_min: int = 16
     split_max: int = 64
     target_tasks: int = 512
+    policy: int = 0
 
 
 def _ceil_div(a: int, b: int) -> int:
@@ -41,15 +48,34 @@ def _ceil_div(a: int, b: int) -> int:
 
 
 def choose_split_count(seq_lens, p: PlanParams) -> int:
-    """Workqueue split count S from the active batch size (Sec. 3.5)."""
+    """Workqueue split count S from the active batch size (Sec. 3.5), policy 0."""
     active = sum(1 for n in seq_lens if int(n) > 0)
     s = _ceil_div(p.target_tasks, max(1, active * p.num_kv_heads))
     return int(min(max(s, p.split_min), p.split_max))
 
 
+def tile_quota(seq_lens, p: PlanParams) -> int:
+    """Tiles per split Q of policy 1: the batch's tiles shared over target_tasks / Hkv
+    splits per KV head, capped so the longest row still gets about split_min splits."""
+    tiles = [_ceil_div(int(n), p.tile_tokens) for n in seq_lens]
+    per_head = max(1, p.target_tasks // p.num_kv_heads)
+    q = max(1, _ceil_div(sum(tiles), per_head))
+    return int(min(q, max(1, _ceil_div(max(tiles, default=0), p.split_min))))
+
+
+def row_split_counts(seq_lens, p: PlanParams):
+    """(nsplit per row, the policy's scalar: S for policy 0, Q for policy 1)."""
+    tiles = [_ceil_div(int(n), p.tile_tokens) for n in seq_lens]
+    if p.policy == 0:
+        S = choose_split_count(seq_lens, p)
+        return [min(S, t) for t in tiles], S
+    Q = tile_quota(seq_lens, p)
+    return [min(p.split_max, _ceil_div(t, Q)) for t in tiles], Q
+
+
 def row_split_bounds(n: int, nsplit_cap: int, tile_tokens: int):
     """Token bounds [(t_begin, t_end)] of the non-empty splits of one row of length n
-    when at most `nsplit_cap` splits are allowed (balanced tile ranges)."""
+    cut into min(nsplit_cap, tiles) balanced tile ranges."""
     tiles = _ceil_div(int(n), tile_tokens)
     k = min(int(nsplit_cap), tiles)
     out = []
@@ -65,6 +91,8 @@ def _validate(seq_lens, p: PlanParams, max_pages_per_row: int | None):
         raise ValueError("tile_tokens must be a positive multiple of page_size")
     if not (1 <= p.split_min <= p.split_max):
         raise ValueError("need 1 <= split_min <= split_max")
+    if p.policy not in (0, 1):
+        raise ValueError("unknown split policy")
     for n in seq_lens:
         if int(n) < 0:
             raise ValueError("negative sequence length")
@@ -73,14 +101,14 @@ def _validate(seq_lens, p: PlanParams, max_pages_per_row: int | None):
 
 
 def ref_plan(seq_lens, p: PlanParams, max_pages_per_row: int | None = None):
-    """Returns (tasks int32 [num_tasks, 5], split_offsets int32 [B+1], S)."""
+    """Returns (tasks int32 [num_tasks, 5], split_offsets int32 [B+1], S or Q)."""
     seq_lens = [int(x) for x in np.asarray(seq_lens).reshape(-1)]
     _validate(seq_lens, p, max_pages_per_row)
-    S = choose_split_count(seq_lens, p)
+    nsplit, S = row_split_counts(seq_lens, p)
     tasks = []
     offsets = [0]
     for i, n in enumerate(seq_lens):
-        bounds = row_split_bounds(n, S, p.tile_tokens)
+        bounds = row_split_bounds(n, nsplit[i], p.tile_tokens)
         for s, (t0, t1) in enumerate(bounds):
             for g in range(p.num_kv_heads):
                 tasks.append((i, g, s, t0, t1))

@@ -5,6 +5,7 @@ behind the C ABI of include/pkv.h); this package is its Python binding.
 """
 from ._binding import (  # noqa: F401
     PKV_DEVERR_PAGE_ID,
+    PKV_DEVERR_PLAN_WAIT,
     PKV_DEVERR_SEQ_LEN,
     PKV_DEVERR_TASK,
     PKV_ERR_DEVICE,
@@ -14,6 +15,8 @@ from ._binding import (  # noqa: F401
     PKV_ERR_WORKSPACE,
     PKV_FUSED_MERGE,
     PKV_OK,
+    PKV_SPLIT_BATCH,
+    PKV_SPLIT_QUOTA,
     DecodeBuffers,
     PkvError,
     PlanParams,
@@ -25,6 +28,7 @@ from ._binding import (  # noqa: F401
     pkv_decode_rect,
     pkv_max_tasks,
     pkv_plan,
+    pkv_plan_decode,
     pkv_stream_copy,
     pkv_stream_read,
     pkv_workspace_init,

@@ -25,7 +25,10 @@ PKV_ERR_DEVICE = 5
 PKV_DEVERR_SEQ_LEN = 1
 PKV_DEVERR_PAGE_ID = 2
 PKV_DEVERR_TASK = 4
+PKV_DEVERR_PLAN_WAIT = 8
 PKV_FUSED_MERGE = 1
+PKV_SPLIT_BATCH = 0
+PKV_SPLIT_QUOTA = 1
 TASK_FIELDS = 5  # row, kvh, split, t_begin, t_end
 
 
@@ -38,7 +41,7 @@ class PkvError(RuntimeError):
 class PlanParams(ctypes.Structure):
     _fields_ = [("page_size", ctypes.c_int32), ("tile_tokens", ctypes.c_int32),
                 ("num_kv_heads", ctypes.c_int32), ("split_min", ctypes.c_int32),
-                ("split_max", ctypes.c_int32), ("target_tasks", ctypes.c_int32)]
+                ("split_max", ctypes.c_int32), ("target_tasks", ctypes.c_int32), ("policy", ctypes.c_int32)]
 
 
 _lib = None
@@ -51,6 +54,8 @@ _SIGS = {
                                 _P, _SZ, _P]),
     "pkv_decode": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _P, _P, _I32,
                                   _F32, _I32, _P, _P, _SZ, _P]),
+    "pkv_plan_decode": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
+                                       ctypes.POINTER(PlanParams), _P, _I32, _P, _P, _F32, _P, _P, _SZ, _P]),
     "pkv_decode_rect": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _I32, _I32,
                                        _F32, _P, _P, _SZ, _P]),
     "pkv_check_device_status": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_uint32)]),
@@ -116,8 +121,8 @@ def pkv_workspace_init(ws: torch.Tensor, B: int, Hkv: int, stream=None):
 
 
 def make_params(num_kv_heads: int, split_min: int, split_max: int, target_tasks: int,
-                tile_tokens: int = 32, page_size: int = 16) -> PlanParams:
-    return PlanParams(page_size, tile_tokens, num_kv_heads, split_min, split_max, target_tasks)
+                tile_tokens: int = 32, page_size: int = 16, policy: int = 0) -> PlanParams:
+    return PlanParams(page_size, tile_tokens, num_kv_heads, split_min, split_max, target_tasks, policy)
 
 
 def pkv_plan(seq_lens: torch.Tensor, block_table, num_pages: int, params: PlanParams, tasks: torch.Tensor,
@@ -149,6 +154,21 @@ def pkv_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, bl
         _dev(num_tasks, torch.int32, "num_tasks"), tasks.numel() // TASK_FIELDS, float(sm_scale),
         PKV_FUSED_MERGE if fused else 0, _dev(out, torch.float16, "out"), _dev(ws, torch.uint8, "ws"),
         ws.numel(), _stream(stream)))
+
+
+def pkv_plan_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
+                    seq_lens: torch.Tensor, params: PlanParams, tasks: torch.Tensor, split_offsets: torch.Tensor,
+                    num_tasks: torch.Tensor, sm_scale: float, out: torch.Tensor, ws: torch.Tensor, *, stream=None):
+    B, Hq, d = q.shape
+    num_pages, _, Hkv, _ = k_cache.shape
+    _check("pkv_plan_decode", lib().pkv_plan_decode(
+        _dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
+        _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
+        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d, ctypes.byref(params),
+        _dev(tasks, torch.int32, "tasks"), tasks.numel() // TASK_FIELDS, _dev(split_offsets, torch.int32,
+                                                                                "split_offsets"),
+        _dev(num_tasks, torch.int32, "num_tasks"), float(sm_scale), _dev(out, torch.float16, "out"),
+        _dev(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
 
 
 def pkv_decode_rect(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,

@@ -3,6 +3,7 @@
 // leaves the stream untouched.
 #include <hip/hip_runtime_api.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -62,6 +63,50 @@ DecodeArgs make_args(const uint16_t* q, const uint16_t* k, const uint16_t* v, in
   return a;
 }
 
+int make_plan_args(const int32_t* seq_lens, const int32_t* block_table, int32_t B, int32_t max_pages_per_row,
+                   int32_t num_pages, const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+                   int32_t* split_offsets, int32_t* num_tasks, void* ws, size_t ws_bytes, PlanArgs* out) {
+  if (!seq_lens || !params || !tasks || !split_offsets || !num_tasks || !ws) return PKV_ERR_INVALID_ARG;
+  if (B < 1 || B > kMaxPlanBatch || max_pages_per_row < 1) return PKV_ERR_INVALID_ARG;
+  if (block_table && num_pages < 1) return PKV_ERR_INVALID_ARG;
+  if (!aligned(ws, 16) || !aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
+  const pkv_plan_params p = *params;
+  if (p.page_size != kPageSize) return PKV_ERR_UNSUPPORTED;
+  if (p.tile_tokens <= 0 || p.tile_tokens % p.page_size != 0) return PKV_ERR_UNSUPPORTED;
+  if (p.num_kv_heads < 1 || p.split_min < 1 || p.split_min > p.split_max || p.target_tasks < 1)
+    return PKV_ERR_INVALID_ARG;
+  if (p.policy != PKV_SPLIT_BATCH && p.policy != PKV_SPLIT_QUOTA) return PKV_ERR_INVALID_ARG;
+  if ((int64_t)max_pages_per_row * p.page_size > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  const int32_t bound = pkv_max_tasks(B, p.num_kv_heads, p.split_max);
+  if (bound < 0) return PKV_ERR_INVALID_ARG;
+  if (max_tasks < bound) return PKV_ERR_WORKSPACE;
+  if (ws_bytes < partials_offset(B, p.num_kv_heads)) return PKV_ERR_WORKSPACE;
+  PlanArgs& a = *out;
+  std::memset(&a, 0, sizeof(a));
+  a.seq_lens = seq_lens;
+  a.block_table = block_table;
+  a.B = B;
+  a.max_pages_per_row = max_pages_per_row;
+  a.num_pages = num_pages;
+  a.page_size = p.page_size;
+  a.tile_tokens = p.tile_tokens;
+  a.Hkv = p.num_kv_heads;
+  a.split_min = p.split_min;
+  a.split_max = p.split_max;
+  a.target_tasks = p.target_tasks;
+  a.policy = p.policy;
+  a.tasks = tasks;
+  a.max_tasks = max_tasks;
+  a.split_offsets = split_offsets;
+  a.num_tasks = num_tasks;
+  a.err = reinterpret_cast<unsigned*>(ws);
+  a.counters = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kWsHeaderBytes);
+  return PKV_OK;
+}
+
+// Unique per launch: the plan-ready flag of a fused plan + decode launch holds it.
+std::atomic<unsigned long long> g_launch_token{1};
+
 }  // namespace
 
 extern "C" {
@@ -88,38 +133,10 @@ int pkv_workspace_init(void* ws, size_t ws_bytes, int32_t B, int32_t Hkv, hipStr
 int pkv_plan(const int32_t* seq_lens, const int32_t* block_table, int32_t B, int32_t max_pages_per_row,
              int32_t num_pages, const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
              int32_t* split_offsets, int32_t* num_tasks, void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!seq_lens || !params || !tasks || !split_offsets || !num_tasks || !ws) return PKV_ERR_INVALID_ARG;
-  if (B < 1 || B > kMaxPlanBatch || max_pages_per_row < 1) return PKV_ERR_INVALID_ARG;
-  if (block_table && num_pages < 1) return PKV_ERR_INVALID_ARG;
-  if (!aligned(ws, 16) || !aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
-  const pkv_plan_params p = *params;
-  if (p.page_size != kPageSize) return PKV_ERR_UNSUPPORTED;
-  if (p.tile_tokens <= 0 || p.tile_tokens % p.page_size != 0) return PKV_ERR_UNSUPPORTED;
-  if (p.num_kv_heads < 1 || p.split_min < 1 || p.split_min > p.split_max || p.target_tasks < 1)
-    return PKV_ERR_INVALID_ARG;
-  if ((int64_t)max_pages_per_row * p.page_size > INT32_MAX) return PKV_ERR_INVALID_ARG;
-  const int32_t bound = pkv_max_tasks(B, p.num_kv_heads, p.split_max);
-  if (bound < 0) return PKV_ERR_INVALID_ARG;
-  if (max_tasks < bound) return PKV_ERR_WORKSPACE;
-  if (ws_bytes < partials_offset(B, p.num_kv_heads)) return PKV_ERR_WORKSPACE;
   PlanArgs a;
-  a.seq_lens = seq_lens;
-  a.block_table = block_table;
-  a.B = B;
-  a.max_pages_per_row = max_pages_per_row;
-  a.num_pages = num_pages;
-  a.page_size = p.page_size;
-  a.tile_tokens = p.tile_tokens;
-  a.Hkv = p.num_kv_heads;
-  a.split_min = p.split_min;
-  a.split_max = p.split_max;
-  a.target_tasks = p.target_tasks;
-  a.tasks = tasks;
-  a.max_tasks = max_tasks;
-  a.split_offsets = split_offsets;
-  a.num_tasks = num_tasks;
-  a.err = reinterpret_cast<unsigned*>(ws);
-  a.counters = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kWsHeaderBytes);
+  const int st = make_plan_args(seq_lens, block_table, B, max_pages_per_row, num_pages, params, tasks, max_tasks,
+                                split_offsets, num_tasks, ws, ws_bytes, &a);
+  if (st != PKV_OK) return st;
   return from_hip(launch_plan(a, stream));
 }
 
@@ -201,6 +218,36 @@ int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream
 int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream) {
   if (!src || !sink || bytes % 16 != 0 || !aligned(src, 16) || !aligned(sink, 4)) return PKV_ERR_INVALID_ARG;
   return from_hip(launch_read(src, bytes, sink, stream));
+}
+
+int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                    const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
+                    int32_t Hq, int32_t Hkv, int32_t d, const pkv_plan_params* params, pkv_task* tasks,
+                    int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
+                    void* ws, size_t ws_bytes, hipStream_t stream) {
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
+  if (st != PKV_OK) return st;
+  int G = 0;
+  if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
+  if (!std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
+  if (B > kMaxFusedPlanBatch) return PKV_ERR_UNSUPPORTED;
+  if (params && params->num_kv_heads != Hkv) return PKV_ERR_INVALID_ARG;
+  PlanArgs pa;
+  if ((st = make_plan_args(seq_lens, nullptr, B, max_pages_per_row, num_pages, params, tasks, max_tasks,
+                           split_offsets, num_tasks, ws, ws_bytes, &pa)) != PKV_OK)
+    return st;
+  if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, max_tasks)) return PKV_ERR_WORKSPACE;
+  if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
+                           Hkv, sm_scale, out, ws);
+  a.tasks = tasks;
+  a.split_offsets = split_offsets;
+  a.num_tasks = num_tasks;
+  a.max_tasks = max_tasks;
+  a.plan = pa;
+  a.ready = reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) + kWsReadyOffset);
+  a.token = g_launch_token.fetch_add(1);
+  return from_hip(launch_decode(a, G, 3, max_tasks, stream));
 }
 
 }  // extern "C"

@@ -12,6 +12,8 @@ namespace pkv {
 constexpr int kHeadDim = 128;
 constexpr int kPageSize = 16;
 constexpr int kMaxPlanBatch = 4096;
+constexpr int kMaxFusedPlanBatch = 1024;
+constexpr size_t kWsReadyOffset = 64;  // plan-ready flag inside the workspace header
 constexpr size_t kWsHeaderBytes = 256;
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -19,6 +21,19 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 inline size_t slot_floats(int G) { return size_t(G * kHeadDim + ((2 * G + 3) / 4) * 4); }
 inline size_t counters_bytes(int B, int Hkv) { return align256(size_t(B) * size_t(Hkv) * 4); }
 inline size_t partials_offset(int B, int Hkv) { return kWsHeaderBytes + counters_bytes(B, Hkv); }
+
+struct PlanArgs {
+  const int32_t* seq_lens;
+  const int32_t* block_table;
+  int32_t B, max_pages_per_row, num_pages;
+  int32_t page_size, tile_tokens, Hkv, split_min, split_max, target_tasks, policy;
+  pkv_task* tasks;
+  int32_t max_tasks;
+  int32_t* split_offsets;
+  int32_t* num_tasks;
+  unsigned* err;
+  int32_t* counters;
+};
 
 struct DecodeArgs {
   const uint16_t* q;
@@ -40,23 +55,16 @@ struct DecodeArgs {
   int32_t S;            // rectangular route only
   int32_t tile_tokens;  // rectangular route only
   float scale_log2;     // sm_scale * log2(e)
+  // planning inside the decode launch (pkv_plan_decode)
+  PlanArgs plan;
+  unsigned long long* ready;  // flag in the workspace header
+  unsigned long long token;   // unique per launch
 };
 
-struct PlanArgs {
-  const int32_t* seq_lens;
-  const int32_t* block_table;
-  int32_t B, max_pages_per_row, num_pages;
-  int32_t page_size, tile_tokens, Hkv, split_min, split_max, target_tasks;
-  pkv_task* tasks;
-  int32_t max_tasks;
-  int32_t* split_offsets;
-  int32_t* num_tasks;
-  unsigned* err;
-  int32_t* counters;
-};
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
-// mode: 0 split + merge kernels, 1 fused merge, 2 rectangular split + merge
+// mode: 0 split + merge kernels, 1 fused merge, 2 rectangular split + merge,
+//       3 plan + split + fused merge in one launch
 hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);

@@ -527,23 +527,253 @@ constexpr int lds_floats() {
   return 2 * W * G + W * G * D + W;
 }
 
+// ---------------------------------------------------------------------------------
+// Planner (Sec. 3.4), run by one workgroup. Lengths are validated; each row gets
+// nsplit_i splits (policy 0: min(S, tiles_i) with S from the active batch size;
+// policy 1: min(split_max, ceil(tiles_i / Q)) with a tile quota Q from the batch's
+// total tiles); split_offsets is their exclusive scan, and task
+// k = (split_offsets[i] + s) * Hkv + g covers the balanced tile range
+// [floor(s*tiles/nsplit), floor((s+1)*tiles/nsplit)) of row i.
+constexpr int kPlanThreads = 256;
+
+// inclusive prefix sum over the 64 lanes of a wave
+__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ int wave_sum(int x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+__device__ __forceinline__ long long wave_sum64(long long x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+__device__ __forceinline__ int wave_max(int x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x = max(x, __shfl_xor(x, off));
+  return x;
+}
+
+// Plan outputs read in the same kernel by other workgroups go out with agent-scope
+// stores (see the partial-state slots) and are read back with agent-scope loads.
+template <bool COHERENT>
+__device__ __forceinline__ void st_i32(int* p, int v) {
+  if (COHERENT) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else *p = v;
+}
+template <bool COHERENT>
+__device__ __forceinline__ int ld_i32(const int* p) {
+  if (COHERENT) return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return *p;
+}
+
+struct PlanLds {
+  int* len;        // [B]
+  int* off;        // [B + 1]
+  int* wave;       // [NT / 64]
+  long long* w64;  // [NT / 64]
+  int* wmax;       // [NT / 64]
+};
+
+template <int NT, bool COHERENT>
+__device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
+  constexpr int NW = NT / 64;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int B = a.B;
+  const int cap = a.max_pages_per_row * a.page_size;
+  const int T = a.tile_tokens;
+  // 1. validated lengths; each thread owns the contiguous rows [r0, r0 + per)
+  const int per = (B + NT - 1) / NT;
+  const int r0 = tid * per;
+  for (int i = r0; i < r0 + per && i < B; ++i) {
+    int n = a.seq_lens[i];
+    if (n < 0 || n > cap) {
+      atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
+      n = 0;
+    }
+    L.len[i] = n;
+  }
+  if (a.block_table) {  // optional: drop rows whose used block-table entries are out of range
+    __syncthreads();
+    const long long total = (long long)B * a.max_pages_per_row;
+    for (long long k = tid; k < total; k += NT) {
+      const int i = (int)(k / a.max_pages_per_row);
+      const int jp = (int)(k % a.max_pages_per_row);
+      if (jp < (L.len[i] + a.page_size - 1) / a.page_size) {
+        const int phys = a.block_table[k];
+        if (phys < 0 || phys >= a.num_pages) {
+          atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
+          L.len[i] = 0;  // benign race: every writer stores 0
+        }
+      }
+    }
+    __syncthreads();
+  }
+  int act = 0;
+  long long tsum = 0;
+  int tmax = 0;
+  for (int i = r0; i < r0 + per && i < B; ++i) {
+    const int tiles = (L.len[i] + T - 1) / T;
+    act += tiles > 0;
+    tsum += tiles;
+    tmax = max(tmax, tiles);
+  }
+  // 2. batch-level quantities: active rows, total and largest tile count
+  act = wave_sum(act);
+  tsum = wave_sum64(tsum);
+  tmax = wave_max(tmax);
+  if (lane == 0) {
+    L.wave[wave] = act;
+    L.w64[wave] = tsum;
+    L.wmax[wave] = tmax;
+  }
+  __syncthreads();
+  int active = 0;
+  long long total_tiles = 0;
+  int max_tiles = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    active += L.wave[w];
+    total_tiles += L.w64[w];
+    max_tiles = max(max_tiles, L.wmax[w]);
+  }
+  // policy 0: one split count S from the active batch size (Sec. 3.5);
+  // policy 1: a tile quota Q per split from the batch's total work
+  long long S = 0, Q = 1;
+  if (a.policy == 0) {
+    const long long denom = (long long)(active > 0 ? active : 1) * a.Hkv;
+    S = (a.target_tasks + denom - 1) / denom;
+    if (S < a.split_min) S = a.split_min;
+    if (S > a.split_max) S = a.split_max;
+  } else {
+    const long long per_head = max(1, a.target_tasks / a.Hkv);
+    Q = (total_tiles + per_head - 1) / per_head;
+    if (Q < 1) Q = 1;
+    const long long qcap = max(1LL, ((long long)max_tiles + a.split_min - 1) / a.split_min);
+    if (Q > qcap) Q = qcap;
+  }
+  auto row_nsplit = [&](int n) -> int {
+    const int tiles = (n + T - 1) / T;
+    if (a.policy == 0) return (int)min((long long)tiles, S);
+    return (int)min((long long)a.split_max, (tiles + Q - 1) / Q);
+  };
+  // 3. exclusive scan of nsplit over rows -> split_offsets
+  int local = 0;
+  for (int i = r0; i < r0 + per && i < B; ++i) local += row_nsplit(L.len[i]);
+  const int incl = wave_incl_scan(local, lane);
+  __syncthreads();  // every wave has read L.wave
+  if (lane == 63) L.wave[wave] = incl;
+  __syncthreads();
+  int run = incl - local;
+  for (int w = 0; w < wave; ++w) run += L.wave[w];
+  for (int i = r0; i < r0 + per && i < B; ++i) {
+    L.off[i] = run;
+    run += row_nsplit(L.len[i]);
+  }
+  if (tid == NT - 1) L.off[B] = run;
+  __syncthreads();
+  for (int i = tid; i <= B; i += NT) st_i32<COHERENT>(a.split_offsets + i, L.off[i]);
+  long long ntasks = (long long)L.off[B] * a.Hkv;
+  if (ntasks > a.max_tasks) {  // excluded by host validation; never write past the buffer
+    if (tid == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
+    ntasks = 0;
+  }
+  if (tid == 0) st_i32<COHERENT>(a.num_tasks, (int)ntasks);
+  // 4. task k = (split_offsets[i] + s) * Hkv + g: balanced tile range s of row i
+  for (int k = tid; k < (int)ntasks; k += NT) {
+    const int sr = k / a.Hkv;
+    const int g = k % a.Hkv;
+    int lo = 0, hi = B;  // largest i with off[i] <= sr
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (L.off[mid] <= sr) lo = mid; else hi = mid;
+    }
+    const int i = lo;
+    const int sp = sr - L.off[i];
+    const int n = L.len[i];
+    const int tiles = (n + T - 1) / T;
+    const int ns = L.off[i + 1] - L.off[i];
+    const int b0 = (int)(((long long)sp * tiles) / ns);
+    const int b1 = (int)(((long long)(sp + 1) * tiles) / ns);
+    int* t = reinterpret_cast<int*>(a.tasks + k);
+    st_i32<COHERENT>(t + 0, i);
+    st_i32<COHERENT>(t + 1, g);
+    st_i32<COHERENT>(t + 2, sp);
+    st_i32<COHERENT>(t + 3, b0 * T);
+    st_i32<COHERENT>(t + 4, min(b1 * T, n));
+  }
+  for (int k = tid; k < B * a.Hkv; k += NT) st_i32<COHERENT>(a.counters + k, 0);
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
+  __shared__ int s_len[kMaxPlanBatch];
+  __shared__ int s_off[kMaxPlanBatch + 1];
+  __shared__ int s_wave[kPlanThreads / 64];
+  __shared__ long long s_w64[kPlanThreads / 64];
+  __shared__ int s_wmax[kPlanThreads / 64];
+  plan_body<kPlanThreads, false>(a, PlanLds{s_len, s_off, s_wave, s_w64, s_wmax});
+}
+
 // Workqueue split kernel. FUSED: the last split of each (row, KV head) to finish merges
 // all of that pair's splits in split order (Sec. 3.4, atomic completion counter).
-template <int G, int W, bool FUSED>
+// PLAN: workgroup 0 first builds the task list (the planner above) and publishes it
+// through a flag holding this launch's token; the other workgroups wait for the token.
+// Workgroup 0 is dispatched first and never waits, so the wait always ends; a bounded
+// spin turns a missing token into an error instead of a hang.
+constexpr int kSpinLimit = 1 << 24;
+
+template <int G, int W, bool FUSED, bool PLAN>
 __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   __shared__ float lds[lds_floats<G, W>()];
   __shared__ float lds_merge[FUSED ? merge_lds_floats<G>() : 1];
   __shared__ int lds_last;
+  __shared__ int p_len[PLAN ? kMaxFusedPlanBatch : 1];
+  __shared__ int p_off[PLAN ? kMaxFusedPlanBatch + 1 : 1];
+  __shared__ int p_wave[W];
+  __shared__ long long p_w64[W];
+  __shared__ int p_wmax[W];
+  if (PLAN) {
+    if (blockIdx.x == 0) {
+      plan_body<W * 64, true>(a.plan, PlanLds{p_len, p_off, p_wave, p_w64, p_wmax});
+      __builtin_amdgcn_s_waitcnt(0);  // every plan store acknowledged
+      __syncthreads();
+      if (threadIdx.x == 0) __hip_atomic_store(a.ready, a.token, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      if (threadIdx.x == 0) {
+        int spins = 0;
+        while (__hip_atomic_load(a.ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.token &&
+               ++spins < kSpinLimit)
+          __builtin_amdgcn_s_sleep(2);
+        lds_last = spins < kSpinLimit;
+        if (!lds_last) atomicOr(a.err, (unsigned)PKV_DEVERR_PLAN_WAIT);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      }
+      __syncthreads();
+      if (!lds_last) return;
+    }
+  }
   if (FUSED) {
     for (int i = blockIdx.x; i < a.B; i += gridDim.x)
-      if (a.split_offsets[i + 1] == a.split_offsets[i]) zero_row<G>(a, i);
+      if (ld_i32<PLAN>(a.split_offsets + i + 1) == ld_i32<PLAN>(a.split_offsets + i)) zero_row<G>(a, i);
   }
-  int ntasks = uniform(*a.num_tasks);
+  int ntasks = uniform(ld_i32<PLAN>(a.num_tasks));
   if (ntasks > a.max_tasks) ntasks = a.max_tasks;
   for (int t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const pkv_task task = a.tasks[t];
-    const int row = uniform(task.row), g = uniform(task.kvh);
-    const int t0 = uniform(task.t_begin), t1 = uniform(task.t_end);
+    const int* tp = reinterpret_cast<const int*>(a.tasks + t);
+    const int row = uniform(ld_i32<PLAN>(tp + 0)), g = uniform(ld_i32<PLAN>(tp + 1));
+    const int t0 = uniform(ld_i32<PLAN>(tp + 3)), t1 = uniform(ld_i32<PLAN>(tp + 4));
     if (row < 0 || row >= a.B || g < 0 || g >= a.Hkv || t0 < 0 || t1 <= t0 ||
         t1 > a.max_pages_per_row * P) {  // not a task of a valid plan: flag and skip
       if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
@@ -551,8 +781,8 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
     }
     run_task<G, W, FUSED>(a, row, g, t0, t1, t, lds);
     if (FUSED) {
-      const int off = uniform(a.split_offsets[row]);
-      int nsplit = uniform(a.split_offsets[row + 1]) - off;
+      const int off = uniform(ld_i32<PLAN>(a.split_offsets + row));
+      int nsplit = uniform(ld_i32<PLAN>(a.split_offsets + row + 1)) - off;
       if (off < 0 || nsplit < 1 || (long long)(off + nsplit) * a.Hkv > a.max_tasks) {
         if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
         nsplit = 0;  // never reached by the counter: no merge from inconsistent offsets
@@ -635,114 +865,6 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
                                 a.out + ((size_t)row * a.Hq + (size_t)g * G) * D, lds);
 }
 
-// ---------------------------------------------------------------------------------
-// Planner (Sec. 3.4): one workgroup. Lengths are validated, S follows the active batch
-// size, nsplit_i = min(S, ceil(N_i / T)), split_offsets is their exclusive scan, and
-// task k = (split_offsets[i] + s) * Hkv + g covers the balanced tile range
-// [floor(s*tiles/nsplit), floor((s+1)*tiles/nsplit)) of row i.
-constexpr int kPlanThreads = 1024;
-
-__global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
-  __shared__ int s_len[kMaxPlanBatch];
-  __shared__ int s_off[kMaxPlanBatch + 1];
-  __shared__ int s_scan[kPlanThreads];
-  __shared__ int s_active;
-  const int tid = threadIdx.x;
-  const int B = a.B;
-  const int cap = a.max_pages_per_row * a.page_size;
-  if (tid == 0) s_active = 0;
-  for (int i = tid; i < B; i += kPlanThreads) {
-    int n = a.seq_lens[i];
-    if (n < 0 || n > cap) {
-      atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
-      n = 0;
-    }
-    s_len[i] = n;
-  }
-  __syncthreads();
-  if (a.block_table) {
-    const long long total = (long long)B * a.max_pages_per_row;
-    for (long long k = tid; k < total; k += kPlanThreads) {
-      const int i = (int)(k / a.max_pages_per_row);
-      const int jp = (int)(k % a.max_pages_per_row);
-      const int n = s_len[i];
-      if (jp < (n + a.page_size - 1) / a.page_size) {
-        const int phys = a.block_table[k];
-        if (phys < 0 || phys >= a.num_pages) {
-          atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
-          s_len[i] = 0;  // benign race: every writer stores 0
-        }
-      }
-    }
-    __syncthreads();
-  }
-  int act = 0;
-  for (int i = tid; i < B; i += kPlanThreads) act += s_len[i] > 0;
-  if (act) atomicAdd(&s_active, act);
-  __syncthreads();
-  const int T = a.tile_tokens;
-  const long long denom = (long long)(s_active > 0 ? s_active : 1) * a.Hkv;
-  long long Sll = (a.target_tasks + denom - 1) / denom;
-  if (Sll < a.split_min) Sll = a.split_min;
-  if (Sll > a.split_max) Sll = a.split_max;
-  const int S = (int)Sll;
-
-  // exclusive scan of nsplit over rows: thread tid owns rows [tid*per, (tid+1)*per)
-  const int per = (B + kPlanThreads - 1) / kPlanThreads;
-  const int r0 = tid * per;
-  int local = 0;
-  for (int i = r0; i < r0 + per && i < B; ++i) {
-    const int tiles = (s_len[i] + T - 1) / T;
-    local += tiles < S ? tiles : S;
-  }
-  s_scan[tid] = local;
-  __syncthreads();
-  for (int off = 1; off < kPlanThreads; off <<= 1) {
-    const int v = tid >= off ? s_scan[tid - off] : 0;
-    __syncthreads();
-    s_scan[tid] += v;
-    __syncthreads();
-  }
-  int run = s_scan[tid] - local;  // exclusive prefix
-  for (int i = r0; i < r0 + per && i < B; ++i) {
-    s_off[i] = run;
-    const int tiles = (s_len[i] + T - 1) / T;
-    run += tiles < S ? tiles : S;
-  }
-  if (tid == kPlanThreads - 1) s_off[B] = s_scan[kPlanThreads - 1];
-  __syncthreads();
-  for (int i = tid; i <= B; i += kPlanThreads) a.split_offsets[i] = s_off[i];
-  long long ntasks = (long long)s_off[B] * a.Hkv;
-  if (ntasks > a.max_tasks) {  // excluded by host validation; never write past the buffer
-    if (tid == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
-    ntasks = 0;
-  }
-  if (tid == 0) *a.num_tasks = (int)ntasks;
-  for (int k = tid; k < (int)ntasks; k += kPlanThreads) {
-    const int sr = k / a.Hkv;
-    const int g = k % a.Hkv;
-    int lo = 0, hi = B;  // largest i with s_off[i] <= sr
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (s_off[mid] <= sr) lo = mid; else hi = mid;
-    }
-    const int i = lo;
-    const int s = sr - s_off[i];
-    const int n = s_len[i];
-    const int tiles = (n + T - 1) / T;
-    const int ns = s_off[i + 1] - s_off[i];
-    const int b0 = (int)(((long long)s * tiles) / ns);
-    const int b1 = (int)(((long long)(s + 1) * tiles) / ns);
-    pkv_task* t = a.tasks + k;
-    t->row = i;
-    t->kvh = g;
-    t->split = s;
-    t->t_begin = b0 * T;
-    t->t_end = min(b1 * T, n);
-  }
-  for (int k = tid; k < B * a.Hkv; k += kPlanThreads) a.counters[k] = 0;
-}
-
 __global__ void zero_kernel(uint32_t* p, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = 0u;
 }
@@ -771,10 +893,14 @@ hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t 
     return hipGetLastError();
   }
   if (mode == 1) {
-    hipLaunchKernelGGL((split_kernel<G, W, true>), dim3(grid), dim3(W * 64), 0, s, a);
+    hipLaunchKernelGGL((split_kernel<G, W, true, false>), dim3(grid), dim3(W * 64), 0, s, a);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((split_kernel<G, W, false>), dim3(grid), dim3(W * 64), 0, s, a);
+  if (mode == 3) {
+    hipLaunchKernelGGL((split_kernel<G, W, true, true>), dim3(grid), dim3(W * 64), 0, s, a);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((split_kernel<G, W, false, false>), dim3(grid), dim3(W * 64), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((merge_kernel<G, false>), dim3(a.B * a.Hkv), dim3(kMergeThreads), 0, s, a);

@@ -61,8 +61,8 @@ class Case:
                    block_table=w.block_table, num_pages=w.num_pages), w
 
 
-def plan_params(hkv, split_min=16, split_max=64, target=512, tile=32):
-    return pkv.make_params(hkv, split_min, split_max, target, tile_tokens=tile)
+def plan_params(hkv, split_min=16, split_max=64, target=512, tile=32, policy=0):
+    return pkv.make_params(hkv, split_min, split_max, target, tile_tokens=tile, policy=policy)
 
 
 def run_plan(case, bufs, params, check_pages=False):

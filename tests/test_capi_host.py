@@ -22,7 +22,8 @@ def test_exports_every_header_function():
     L = lib()
     names = pkv.header_functions()
     assert {"pkv_plan", "pkv_decode", "pkv_decode_rect", "pkv_max_tasks", "pkv_workspace_size",
-            "pkv_workspace_init", "pkv_check_device_status", "pkv_status_string", "pkv_stream_copy", "pkv_stream_read"} <= set(names)
+            "pkv_workspace_init", "pkv_check_device_status", "pkv_status_string", "pkv_stream_copy", "pkv_stream_read",
+            "pkv_plan_decode"} <= set(names)
     for n in names:
         assert hasattr(L, n), n
 
@@ -74,6 +75,7 @@ def test_plan_validation():
     assert plan(L, params=b.PlanParams(16, 32, 8, 0, 64, 512)) == pkv.PKV_ERR_INVALID_ARG
     assert plan(L, params=b.PlanParams(16, 32, 0, 16, 64, 512)) == pkv.PKV_ERR_INVALID_ARG
     assert plan(L, params=b.PlanParams(16, 32, 8, 16, 64, 0)) == pkv.PKV_ERR_INVALID_ARG
+    assert plan(L, params=b.PlanParams(16, 32, 8, 16, 64, 512, 2)) == pkv.PKV_ERR_INVALID_ARG  # policy
     assert plan(L, max_tasks=2 * 8 * 64 - 1) == pkv.PKV_ERR_WORKSPACE
     assert plan(L, ws_bytes=511) == pkv.PKV_ERR_WORKSPACE
     assert plan(L, maxp=1 << 28) == pkv.PKV_ERR_INVALID_ARG
@@ -131,3 +133,19 @@ def test_copy_and_init_validation():
     assert L.pkv_workspace_init(FAKE, 100, 1, 8, None) == pkv.PKV_ERR_WORKSPACE
     assert L.pkv_workspace_init(0, 1 << 20, 1, 8, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_check_device_status(0, None, None) == pkv.PKV_ERR_INVALID_ARG
+
+
+def test_plan_decode_validation():
+    L = lib()
+
+    def pd(**kw):
+        a = dict(B=2, d=128, params=b.PlanParams(16, 32, 8, 16, 64, 512), max_tasks=2 * 8 * 64, ws_bytes=1 << 22)
+        a.update(kw)
+        return L.pkv_plan_decode(FAKE, FAKE, FAKE, 100, FAKE, 10, FAKE, a["B"], 32, 8, a["d"],
+                                 ctypes.byref(a["params"]), FAKE, a["max_tasks"], FAKE, FAKE, 1.0, FAKE, FAKE,
+                                 a["ws_bytes"], None)
+    assert pd(B=2000, max_tasks=2000 * 8 * 64) == pkv.PKV_ERR_UNSUPPORTED   # planner inside: B <= 1024
+    assert pd(d=64) == pkv.PKV_ERR_UNSUPPORTED
+    assert pd(params=b.PlanParams(16, 32, 4, 16, 64, 512)) == pkv.PKV_ERR_INVALID_ARG   # Hkv mismatch
+    assert pd(max_tasks=100) == pkv.PKV_ERR_WORKSPACE
+    assert pd(ws_bytes=4096) == pkv.PKV_ERR_WORKSPACE

@@ -26,13 +26,14 @@ def bufs_for(case, split_max=64, rect_splits=0):
 
 def oracle_plan(case, p):
     return ref_plan(case.lens, PlanParams(p.page_size, p.tile_tokens, p.num_kv_heads, p.split_min, p.split_max,
-                                          p.target_tasks), max_pages_per_row=case.bt.shape[1])
+                                          p.target_tasks, p.policy), max_pages_per_row=case.bt.shape[1])
 
 
-@pytest.mark.parametrize("smin,smax,target", [(16, 64, 512), (1, 1, 512), (2, 7, 100), (3, 64, 4096)])
-def test_plan_bit_exact_ragged(smin, smax, target):
+@pytest.mark.parametrize("smin,smax,target,policy", [(16, 64, 512, 0), (1, 1, 512, 0), (2, 7, 100, 0),
+                                                     (3, 64, 4096, 0), (16, 64, 512, 1), (2, 7, 100, 1)])
+def test_plan_bit_exact_ragged(smin, smax, target, policy):
     case = Case(RAGGED, seed=1)
-    p = plan_params(8, smin, smax, target)
+    p = plan_params(8, smin, smax, target, policy=policy)
     bufs = bufs_for(case, smax)
     run_plan(case, bufs, p, check_pages=True)
     tasks, offs = read_plan(bufs)
@@ -42,14 +43,16 @@ def test_plan_bit_exact_ragged(smin, smax, target):
     assert pkv.pkv_check_device_status(bufs.ws) == 0
 
 
+@pytest.mark.parametrize("policy", [0, 1])
 @pytest.mark.parametrize("seed", range(4))
-def test_plan_bit_exact_random_batches(seed):
+def test_plan_bit_exact_random_batches(seed, policy):
     r = np.random.Generator(np.random.PCG64(100 + seed))
     B = int(r.integers(1, 1500))
     lens = r.integers(0, 3000, size=B).astype(np.int32)
     lens[r.random(B) < 0.3] = 0
     case = Case(lens, hkv=int(r.choice([1, 2, 4, 8])), hq=8, seed=seed, rho=0.0, values=False)
-    p = plan_params(case.hkv, int(r.integers(1, 4)), int(r.integers(4, 40)), int(r.integers(1, 20000)))
+    p = plan_params(case.hkv, int(r.integers(1, 4)), int(r.integers(4, 40)), int(r.integers(1, 20000)),
+                    policy=policy)
     bufs = bufs_for(case, p.split_max)
     run_plan(case, bufs, p)
     tasks, offs = read_plan(bufs)
@@ -187,12 +190,13 @@ def test_bad_page_id_is_flagged_and_row_zeroed():
     assert pkv.pkv_check_device_status(bufs.ws) & pkv.PKV_DEVERR_PAGE_ID
 
 
+@pytest.mark.parametrize("policy", [0, 1])
 @pytest.mark.parametrize("name", ["tiny", "b1", "b8_bimodal", "b8_uniform", "b8_zipf", "b4_bimodal"])
-def test_benchmark_configs_full_size(name):
+def test_benchmark_configs_full_size(name, policy):
     """Every output of the first decode step of each benchmark configuration, in the
     launch configuration the benchmark times (planner + fused kernel)."""
     case, w = Case.from_workload(name)
-    p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens)
+    p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens, policy=policy)
     bufs = bufs_for(case, w.split_max)
     run_plan(case, bufs, p)
     tasks, offs = read_plan(bufs)
@@ -217,3 +221,60 @@ def test_b1_last_step_and_uniform_rect():
     wq = run_decode(case, bufs)
     rect = run_rect(case, bufs, 16)
     assert torch.equal(wq, rect)
+
+
+def run_plan_decode(case, bufs, params, sm_scale=1.0):
+    bufs.partial_region().fill_(0xFF)
+    out = torch.full((case.B, case.hq, case.d), float("nan"), dtype=torch.float16, device="cuda")
+    pkv.pkv_plan_decode(case.q_dev, case.k_dev, case.v_dev, case.bt_dev, case.lens_dev, params, bufs.tasks,
+                        bufs.split_offsets, bufs.num_tasks, sm_scale, out, bufs.ws)
+    return out
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_plan_decode_one_launch_equals_plan_then_decode(policy):
+    case = Case(RAGGED, seed=12)
+    p = plan_params(8, 2, 16, 300, policy=policy)
+    ref_bufs = bufs_for(case, 16)
+    run_plan(case, ref_bufs, p)
+    expect = run_decode(case, ref_bufs)
+    tasks_ref, offs_ref = read_plan(ref_bufs)
+    bufs = bufs_for(case, 16)
+    bufs.tasks.fill_(-7)
+    got = run_plan_decode(case, bufs, p)
+    tasks, offs = read_plan(bufs)
+    assert torch.equal(got, expect)
+    assert np.array_equal(tasks, tasks_ref) and np.array_equal(offs, offs_ref)
+    assert np.array_equal(tasks, oracle_plan(case, p)[0])
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+def test_plan_decode_repeated_and_changing_lengths():
+    case = Case([3000, 70, 0, 12000], seed=13)
+    p = plan_params(8, 16, 64, 512)
+    bufs = bufs_for(case)
+    first = run_plan_decode(case, bufs, p)
+    assert_close(first, ref_decode(case.q, case.k, case.v, case.bt, case.lens), "plan_decode")
+    for i in range(100):
+        again = run_plan_decode(case, bufs, p)
+        assert torch.equal(first, again), i
+    # lengths change between calls on the same workspace: the plan follows them
+    lens2 = np.array([2990, 1, 10, 11000], dtype=np.int32)  # row 2 owns one page
+    case.lens_dev = torch.from_numpy(lens2).cuda()
+    out2 = run_plan_decode(case, bufs, p)
+    assert_close(out2, ref_decode(case.q, case.k, case.v, case.bt, lens2), "new lengths")
+    tasks, _ = read_plan(bufs)
+    assert np.array_equal(tasks, ref_plan(lens2, PlanParams(split_min=16, split_max=64, target_tasks=512),
+                                          max_pages_per_row=case.bt.shape[1])[0])
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("name", ["b1", "b8_bimodal"])
+def test_plan_decode_benchmark_configs(name):
+    case, w = Case.from_workload(name)
+    p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens)
+    bufs = bufs_for(case, w.split_max)
+    out = run_plan_decode(case, bufs, p)
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), name)
+    tasks, _ = read_plan(bufs)
+    assert np.array_equal(tasks, oracle_plan(case, p)[0])

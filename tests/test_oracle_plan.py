@@ -38,23 +38,29 @@ def test_balanced_bounds_three_splits_of_seven_tiles():
     assert tasks[:, 3:].tolist() == [[0, 64], [64, 128], [128, 219]]
 
 
+@pytest.mark.parametrize("policy", [0, 1])
 @pytest.mark.parametrize("seed", range(6))
-def test_partition_properties(seed):
+def test_partition_properties(seed, policy):
     r = np.random.Generator(np.random.PCG64(seed))
     B = int(r.integers(1, 12))
     lens = r.integers(0, 5000, size=B)
     lens[r.random(B) < 0.2] = 0
     lo = int(r.integers(1, 8))
     p = PlanParams(num_kv_heads=int(r.integers(1, 9)), split_min=lo, split_max=lo + int(r.integers(0, 40)),
-                   target_tasks=int(r.integers(1, 3000)))
+                   target_tasks=int(r.integers(1, 3000)), policy=policy)
     tasks, offs, S = ref_plan(lens, p)
     T = p.tile_tokens
-    assert p.split_min <= S <= p.split_max
+    if policy == 0:
+        assert p.split_min <= S <= p.split_max
     # brute force over every (row, kv head): the tasks tile [0, N) in split order
     for i, n in enumerate(lens):
         tiles = -(-int(n) // T)
         ns = offs[i + 1] - offs[i]
-        assert ns == min(S, tiles)
+        if policy == 0:
+            assert ns == min(S, tiles)
+        else:  # S holds the tile quota Q: no split exceeds it unless split_max binds
+            assert ns == min(p.split_max, -(-tiles // S))
+            assert ns == 0 or ns == p.split_max or -(-tiles // ns) <= S
         for g in range(p.num_kv_heads):
             mine = [t for t in tasks.tolist() if t[0] == i and t[1] == g]
             assert [t[2] for t in mine] == list(range(ns))
@@ -70,9 +76,39 @@ def test_partition_properties(seed):
                 assert max(sizes) - min(sizes) <= 1
                 assert max(sizes) == -(-tiles // ns)
     # closed-form count and slot order (row, split, kv head) with kv head fastest
-    assert len(tasks) == p.num_kv_heads * sum(min(S, -(-int(n) // T)) for n in lens)
+    if policy == 0:
+        assert len(tasks) == p.num_kv_heads * sum(min(S, -(-int(n) // T)) for n in lens)
     for k, (i, g, s, _, _) in enumerate(tasks.tolist()):
         assert k == (offs[i] + s) * p.num_kv_heads + g
+
+
+def test_quota_policy_hand_worked():
+    # Hkv 2, target 8 -> 4 splits per head; lengths 1000, 100, 0, 3000 -> tiles 32, 4, 0, 94
+    # total 130 -> Q = ceil(130 / 4) = 33; cap ceil(94 / split_min=2) = 47 keeps Q = 33
+    # nsplit = ceil(32/33), ceil(4/33), 0, ceil(94/33) = 1, 1, 0, 3
+    p = PlanParams(num_kv_heads=2, split_min=2, split_max=64, target_tasks=8, policy=1)
+    tasks, offs, Q = ref_plan([1000, 100, 0, 3000], p)
+    assert Q == 33 and offs.tolist() == [0, 1, 2, 2, 5]
+    # row 3: floor(s*94/3) = 0, 31, 62, 94 tiles
+    assert tasks[tasks[:, 0] == 3][::2, 3:].tolist() == [[0, 992], [992, 1984], [1984, 3000]]
+    # the quota cap: one long row and split_min 16 -> at least 16 splits for it
+    p = PlanParams(num_kv_heads=8, split_min=16, split_max=64, target_tasks=8, policy=1)
+    _, offs, Q = ref_plan([32769], p)
+    assert Q == -(-1025 // 16) and offs[1] == 16
+
+
+def test_quota_policy_balances_task_sizes():
+    lens = [1000, 30000, 500, 20000, 2000, 17000, 300, 25000]
+    p = PlanParams(policy=1)
+    tasks, _, Q = ref_plan(lens, p)
+    tiles = (tasks[:, 4] - tasks[:, 3] + 31) // 32
+    assert tiles.max() <= Q
+    # a row with ns = ceil(t / Q) splits has t > Q (ns - 1) tiles, so no piece is smaller
+    # than floor(Q (ns - 1) / ns): long rows are cut into pieces close to Q
+    for i in (1, 3, 5, 7):
+        mine = tiles[tasks[:, 0] == i]
+        ns = len(mine) // 8
+        assert ns > 10 and mine.min() >= (Q * (ns - 1)) // ns
 
 
 def test_split_count_rule():
