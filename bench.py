@@ -288,7 +288,9 @@ def main():
     ap.add_argument("--also", default="b8_bimodal", help="comma-separated extra workloads, or 'none'")
     ap.add_argument("--seed", type=int, default=20260623)
     ap.add_argument("--target-tasks", type=int, default=512)
-    ap.add_argument("--policy", type=int, default=0, help="split policy: 0 batch split count, 1 tile quota")
+    ap.add_argument("--policy", type=int, default=1,
+                    help="split policy: 0 one split count from the active batch size, 1 tile quota (smallest "
+                         "per-split tile quota whose task count fits --target-tasks)")
     ap.add_argument("--route", default="plan+fused", choices=["plan+fused", "one-launch", "two-kernel"],
                     help="plan+fused: planner kernel + fused split/merge kernel (2 launches); one-launch: "
                          "planner inside the decode launch; two-kernel: planner, split kernel, merge kernel")

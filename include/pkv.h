@@ -71,9 +71,10 @@ typedef struct {
  *   PKV_SPLIT_QUOTA  per-row split counts from the step's total work, so that every
  *                    task covers about the same number of tiles (the per-row split
  *                    count the paper names as future work, Sec. 5):
- *                    Q = max(1, ceil(sum tiles_i / max(1, floor(target_tasks / Hkv)))),
- *                    capped at max(1, ceil(max tiles_i / split_min));
- *                    nsplit_i = min(split_max, ceil(tiles_i / Q)) */
+ *                    nsplit_i(Q) = min(split_max, ceil(tiles_i / Q)) with Q the
+ *                    smallest tile quota >= 1 for which Hkv * sum_i nsplit_i(Q) <=
+ *                    target_tasks (max tiles_i if none: one split per row);
+ *                    split_min is not used */
 #define PKV_SPLIT_BATCH 0
 #define PKV_SPLIT_QUOTA 1
 

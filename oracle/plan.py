@@ -16,9 +16,10 @@ boundaries open; the readings taken here are:
     nsplit_i  = min(S, tiles_i)                    (0 for an empty row)
   policy 1 (tile quota: per-row split counts from the batch's total work, so that
             every task covers about the same number of tiles):
-    Q         = max(1, ceil(sum_i tiles_i / max(1, floor(target_tasks / Hkv)))),
-                then Q = min(Q, max(1, ceil(max_i tiles_i / split_min)))
-    nsplit_i  = min(split_max, ceil(tiles_i / Q))  (0 for an empty row)
+    nsplit_i(Q) = min(split_max, ceil(tiles_i / Q))   (0 for an empty row)
+    Q         = the smallest Q >= 1 with Hkv * sum_i nsplit_i(Q) <= target_tasks, or
+                max_i tiles_i when no Q meets it (one split per row); split_min is
+                not used
   split s of row i owns tiles [b_s, b_{s+1}),  b_s = floor(s * tiles_i / nsplit_i)
   task      = (i, g, s, b_s*T, min(b_{s+1}*T, N_i)),  for s < nsplit_i, g < Hkv
   order     = lexicographic in (row, split, kv head), kv head fastest; the task's index
@@ -55,12 +56,15 @@ def choose_split_count(seq_lens, p: PlanParams) -> int:
 
 
 def tile_quota(seq_lens, p: PlanParams) -> int:
-    """Tiles per split Q of policy 1: the batch's tiles shared over target_tasks / Hkv
-    splits per KV head, capped so the longest row still gets about split_min splits."""
+    """Tiles per split Q of policy 1: the smallest quota whose task count fits
+    target_tasks (plain upward search; the count only falls as Q grows)."""
     tiles = [_ceil_div(int(n), p.tile_tokens) for n in seq_lens]
-    per_head = max(1, p.target_tasks // p.num_kv_heads)
-    q = max(1, _ceil_div(sum(tiles), per_head))
-    return int(min(q, max(1, _ceil_div(max(tiles, default=0), p.split_min))))
+    tmax = max(tiles, default=0)
+    for q in range(1, max(tmax, 1) + 1):
+        count = sum(min(p.split_max, _ceil_div(t, q)) for t in tiles)
+        if p.num_kv_heads * count <= p.target_tasks:
+            return q
+    return max(tmax, 1)
 
 
 def row_split_counts(seq_lens, p: PlanParams):

@@ -530,8 +530,8 @@ constexpr int lds_floats() {
 // ---------------------------------------------------------------------------------
 // Planner (Sec. 3.4), run by one workgroup. Lengths are validated; each row gets
 // nsplit_i splits (policy 0: min(S, tiles_i) with S from the active batch size;
-// policy 1: min(split_max, ceil(tiles_i / Q)) with a tile quota Q from the batch's
-// total tiles); split_offsets is their exclusive scan, and task
+// policy 1: min(split_max, ceil(tiles_i / Q)) with the smallest tile quota Q whose task
+// count fits target_tasks); split_offsets is their exclusive scan, and task
 // k = (split_offsets[i] + s) * Hkv + g covers the balanced tile range
 // [floor(s*tiles/nsplit), floor((s+1)*tiles/nsplit)) of row i.
 constexpr int kPlanThreads = 256;
@@ -581,7 +581,7 @@ struct PlanLds {
   int* len;        // [B]
   int* off;        // [B + 1]
   int* wave;       // [NT / 64]
-  long long* w64;  // [NT / 64]
+  long long* w64;  // [2 * NT / 64]
   int* wmax;       // [NT / 64]
 };
 
@@ -658,11 +658,48 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
     if (S < a.split_min) S = a.split_min;
     if (S > a.split_max) S = a.split_max;
   } else {
-    const long long per_head = max(1, a.target_tasks / a.Hkv);
-    Q = (total_tiles + per_head - 1) / per_head;
-    if (Q < 1) Q = 1;
-    const long long qcap = max(1LL, ((long long)max_tiles + a.split_min - 1) / a.split_min);
-    if (Q > qcap) Q = qcap;
+    // smallest Q in [1, max_tiles] with Hkv * sum_i min(split_max, ceil(tiles_i / Q))
+    // <= target_tasks (the count only falls as Q grows), else max_tiles. Bisection;
+    // the upper end starts at ceil(total / (target/Hkv - active)) when that bounds it.
+    const long long per_head = a.target_tasks / a.Hkv;
+    long long hi = max(1, max_tiles);
+    if (per_head > active) hi = min(hi, max(1LL, (total_tiles + per_head - active - 1) / (per_head - active)));
+    long long lo = 1;
+    auto count_local = [&](long long q) {
+      long long c = 0;
+      for (int i = r0; i < r0 + per && i < B; ++i) {
+        const long long t = (L.len[i] + T - 1) / T;
+        c += min((long long)a.split_max, (t + q - 1) / q);
+      }
+      return c;
+    };
+    __syncthreads();  // every wave has read the batch sums in L.w64
+    if (B <= 64) {  // all rows live in wave 0: search without barriers
+      if (wave == 0) {
+        while (lo < hi) {
+          const long long mid = (lo + hi) >> 1;
+          if (wave_sum64(count_local(mid)) <= per_head) hi = mid; else lo = mid + 1;
+        }
+        if (lane == 0) L.w64[0] = lo;
+      }
+      __syncthreads();
+      Q = L.w64[0];
+    } else {
+      int buf = 0;
+      while (lo < hi) {
+        const long long mid = (lo + hi) >> 1;
+        const long long c = wave_sum64(count_local(mid));
+        long long* red = L.w64 + buf * NW;  // two buffers: one barrier per round
+        if (lane == 0) red[wave] = c;
+        __syncthreads();
+        long long tot = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w) tot += red[w];
+        if (tot <= per_head) hi = mid; else lo = mid + 1;
+        buf ^= 1;
+      }
+      Q = lo;
+    }
   }
   auto row_nsplit = [&](int n) -> int {
     const int tiles = (n + T - 1) / T;
@@ -721,7 +758,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
   __shared__ int s_len[kMaxPlanBatch];
   __shared__ int s_off[kMaxPlanBatch + 1];
   __shared__ int s_wave[kPlanThreads / 64];
-  __shared__ long long s_w64[kPlanThreads / 64];
+  __shared__ long long s_w64[2 * kPlanThreads / 64];
   __shared__ int s_wmax[kPlanThreads / 64];
   plan_body<kPlanThreads, false>(a, PlanLds{s_len, s_off, s_wave, s_w64, s_wmax});
 }
@@ -742,7 +779,7 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   __shared__ int p_len[PLAN ? kMaxFusedPlanBatch : 1];
   __shared__ int p_off[PLAN ? kMaxFusedPlanBatch + 1 : 1];
   __shared__ int p_wave[W];
-  __shared__ long long p_w64[W];
+  __shared__ long long p_w64[2 * W];
   __shared__ int p_wmax[W];
   if (PLAN) {
     if (blockIdx.x == 0) {
@@ -764,16 +801,28 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       if (!lds_last) return;
     }
   }
-  if (FUSED) {
-    for (int i = blockIdx.x; i < a.B; i += gridDim.x)
-      if (ld_i32<PLAN>(a.split_offsets + i + 1) == ld_i32<PLAN>(a.split_offsets + i)) zero_row<G>(a, i);
+  // The first task record is fetched together with the task count (the grid never
+  // exceeds max_tasks, so the record lies inside the task buffer even when unused).
+  int rec[4];
+  {
+    const int* tp = reinterpret_cast<const int*>(a.tasks + blockIdx.x);
+    rec[0] = ld_i32<PLAN>(tp + 0);
+    rec[1] = ld_i32<PLAN>(tp + 1);
+    rec[2] = ld_i32<PLAN>(tp + 3);
+    rec[3] = ld_i32<PLAN>(tp + 4);
   }
   int ntasks = uniform(ld_i32<PLAN>(a.num_tasks));
   if (ntasks > a.max_tasks) ntasks = a.max_tasks;
   for (int t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    const int* tp = reinterpret_cast<const int*>(a.tasks + t);
-    const int row = uniform(ld_i32<PLAN>(tp + 0)), g = uniform(ld_i32<PLAN>(tp + 1));
-    const int t0 = uniform(ld_i32<PLAN>(tp + 3)), t1 = uniform(ld_i32<PLAN>(tp + 4));
+    if (t != (int)blockIdx.x) {
+      const int* tp = reinterpret_cast<const int*>(a.tasks + t);
+      rec[0] = ld_i32<PLAN>(tp + 0);
+      rec[1] = ld_i32<PLAN>(tp + 1);
+      rec[2] = ld_i32<PLAN>(tp + 3);
+      rec[3] = ld_i32<PLAN>(tp + 4);
+    }
+    const int row = uniform(rec[0]), g = uniform(rec[1]);
+    const int t0 = uniform(rec[2]), t1 = uniform(rec[3]);
     if (row < 0 || row >= a.B || g < 0 || g >= a.Hkv || t0 < 0 || t1 <= t0 ||
         t1 > a.max_pages_per_row * P) {  // not a task of a valid plan: flag and skip
       if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
@@ -807,6 +856,10 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       }
     }
     __syncthreads();
+  }
+  if (FUSED) {  // rows without tasks: their output is zero
+    for (int i = blockIdx.x; i < a.B; i += gridDim.x)
+      if (ld_i32<PLAN>(a.split_offsets + i + 1) == ld_i32<PLAN>(a.split_offsets + i)) zero_row<G>(a, i);
   }
 }
 

@@ -78,23 +78,36 @@ def test_partition_properties(seed, policy):
     # closed-form count and slot order (row, split, kv head) with kv head fastest
     if policy == 0:
         assert len(tasks) == p.num_kv_heads * sum(min(S, -(-int(n) // T)) for n in lens)
+    else:  # the quota is the smallest that fits the target (or one split per row)
+        def count(q):
+            return p.num_kv_heads * sum(min(p.split_max, -(-(-(-int(n) // T)) // q)) for n in lens)
+        assert len(tasks) == count(S)
+        if S > 1:
+            assert count(S - 1) > p.target_tasks
+        assert len(tasks) <= p.target_tasks or len(tasks) == p.num_kv_heads * sum(1 for n in lens if n > 0)
     for k, (i, g, s, _, _) in enumerate(tasks.tolist()):
         assert k == (offs[i] + s) * p.num_kv_heads + g
 
 
 def test_quota_policy_hand_worked():
-    # Hkv 2, target 8 -> 4 splits per head; lengths 1000, 100, 0, 3000 -> tiles 32, 4, 0, 94
-    # total 130 -> Q = ceil(130 / 4) = 33; cap ceil(94 / split_min=2) = 47 keeps Q = 33
-    # nsplit = ceil(32/33), ceil(4/33), 0, ceil(94/33) = 1, 1, 0, 3
+    # Hkv 2, target 8 -> at most 4 splits summed over rows; tiles 32, 4, 0, 94.
+    # Q = 32: splits 1, 1, 0, 3 = 5 (too many); Q = 47: 1, 1, 0, 2 = 4 fits, and every
+    # Q in 33..46 still gives ceil(94/Q) = 3 -> Q = 47.
     p = PlanParams(num_kv_heads=2, split_min=2, split_max=64, target_tasks=8, policy=1)
     tasks, offs, Q = ref_plan([1000, 100, 0, 3000], p)
-    assert Q == 33 and offs.tolist() == [0, 1, 2, 2, 5]
-    # row 3: floor(s*94/3) = 0, 31, 62, 94 tiles
-    assert tasks[tasks[:, 0] == 3][::2, 3:].tolist() == [[0, 992], [992, 1984], [1984, 3000]]
-    # the quota cap: one long row and split_min 16 -> at least 16 splits for it
-    p = PlanParams(num_kv_heads=8, split_min=16, split_max=64, target_tasks=8, policy=1)
-    _, offs, Q = ref_plan([32769], p)
-    assert Q == -(-1025 // 16) and offs[1] == 16
+    assert Q == 47 and offs.tolist() == [0, 1, 2, 2, 4]
+    # row 3: floor(s*94/2) = 0, 47, 94 tiles
+    assert tasks[tasks[:, 0] == 3][::2, 3:].tolist() == [[0, 1504], [1504, 3000]]
+    # one 32K row, target 512 over 8 heads: at most 64 splits; split_max = 64 caps the
+    # row already at Q = 1, so Q = 1 and the row gets 64 splits
+    _, offs, Q = ref_plan([32769], PlanParams(policy=1))
+    assert Q == 1 and offs[1] == 64
+    # with split_max 100 the cap no longer binds: Q = ceil(1025/64) = 17 -> 61 splits
+    _, offs, Q = ref_plan([32769], PlanParams(policy=1, split_max=100))
+    assert Q == 17 and offs[1] == 61
+    # a target below one split per row: every non-empty row keeps one split
+    tasks, offs, Q = ref_plan([40, 900, 0], PlanParams(num_kv_heads=8, target_tasks=8, policy=1))
+    assert offs.tolist() == [0, 1, 2, 2] and Q == 29
 
 
 def test_quota_policy_balances_task_sizes():
