@@ -168,17 +168,38 @@ int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
                     int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Rectangular split grid (Sec. 3.4): B * Hkv * S split workgroups, then a merge over
- * all S columns (two kernels, no planner). Column s of row i owns the same balanced
- * tile range the planner gives split s when s < min(S, tiles_i); otherwise it writes
- * the neutral state (-inf, 0, 0) and exits before loading Q (Sec. 3.3). With the same
- * S the output is bit-identical to pkv_decode. ws needs max_tasks >= B * Hkv * S;
+/* Rectangular split grid (Sec. 3.4): rows * Hkv * S split workgroups, then a merge over
+ * all S columns (two kernels, no planner). Column s of a row owns the same balanced tile
+ * range the planner gives split s when s < min(S, tiles); otherwise it writes the
+ * neutral state (-inf, 0, 0) and exits before loading Q (Sec. 3.3). The launch covers
+ * rows 0..B-1 when row_ids is NULL, else the n_rows (1..64) rows listed in the HOST
+ * array row_ids, reading Q and writing out by index (indexed Q/O, Sec. 4.6). With the
+ * same S the output is bit-identical to pkv_decode. ws needs max_tasks >= rows * Hkv * S;
  * tile_tokens as in pkv_plan_params. */
 int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
                     int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
                     const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
-                    int32_t S, int32_t tile_tokens, float sm_scale, uint16_t* out, void* ws,
-                    size_t ws_bytes, hipStream_t stream);
+                    const int32_t* row_ids, int32_t n_rows, int32_t S, int32_t tile_tokens,
+                    float sm_scale, uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Length-bucket route (Sec. 3.4, Sec. 4.5): rows grouped on the host by route length
+ * and one pkv_decode_rect launch pair per group, on `stream` in order.
+ *   host_seq_lens  HOST int32 [B], equal to the device seq_lens
+ *   bucket_tokens  0: exact-length buckets (one group per distinct length);
+ *                  > 0: coarse buckets, rows grouped by ceil(len / bucket_tokens) and
+ *                  masked to their own lengths (row-local bounds, Sec. 3.3)
+ *   params         split bounds, target and tile: a group of n rows gets
+ *                  S = clamp(ceil(target_tasks / (n * Hkv)), split_min, split_max)
+ *   launches       optional host output: kernel launches issued (2 per group)
+ * Groups hold at most 64 rows (larger groups are cut). Rows of length 0 form a group
+ * whose output is written as zeros. ws needs max_tasks >= max over groups of
+ * n * Hkv * S. */
+int pkv_decode_buckets(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                       int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                       const int32_t* seq_lens, const int32_t* host_seq_lens, int32_t B, int32_t Hq,
+                       int32_t Hkv, int32_t d, int32_t bucket_tokens, const pkv_plan_params* params,
+                       float sm_scale, uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream,
+                       int32_t* launches);
 
 /* Synchronize `stream`, read the workspace error word into *error_bits (may be NULL)
  * and clear it. Returns PKV_OK when no bit was set, PKV_ERR_DEVICE otherwise. */

@@ -25,6 +25,7 @@ from ._binding import (  # noqa: F401
     make_params,
     pkv_check_device_status,
     pkv_decode,
+    pkv_decode_buckets,
     pkv_decode_rect,
     pkv_max_tasks,
     pkv_plan,

@@ -56,8 +56,11 @@ _SIGS = {
                                   _F32, _I32, _P, _P, _SZ, _P]),
     "pkv_plan_decode": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
                                        ctypes.POINTER(PlanParams), _P, _I32, _P, _P, _F32, _P, _P, _SZ, _P]),
-    "pkv_decode_rect": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _I32, _I32,
-                                       _F32, _P, _P, _SZ, _P]),
+    "pkv_decode_rect": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _I32, _I32,
+                                       _I32, _F32, _P, _P, _SZ, _P]),
+    "pkv_decode_buckets": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _P, _I32, _I32, _I32, _I32, _I32,
+                                          ctypes.POINTER(PlanParams), _F32, _P, _P, _SZ, _P,
+                                          ctypes.POINTER(ctypes.c_int32)]),
     "pkv_check_device_status": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_uint32)]),
     "pkv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "pkv_stream_copy": (ctypes.c_int, [_P, _P, _SZ, _P]),
@@ -171,17 +174,45 @@ def pkv_plan_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tenso
         _dev(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
 
 
+def _host_i32(x) -> tuple:
+    import numpy as np
+    arr = np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+    return arr, arr.ctypes.data_as(ctypes.c_void_p)
+
+
 def pkv_decode_rect(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
                     seq_lens: torch.Tensor, S: int, tile_tokens: int, sm_scale: float, out: torch.Tensor,
-                    ws: torch.Tensor, *, stream=None):
+                    ws: torch.Tensor, *, row_ids=None, stream=None):
+    """row_ids: optional host sequence of at most 64 rows (indexed Q/O)."""
     B, Hq, d = q.shape
     num_pages, _, Hkv, _ = k_cache.shape
+    ids, ids_ptr, n = None, None, 0
+    if row_ids is not None:
+        ids, ids_ptr = _host_i32(row_ids)
+        n = ids.size
     _check("pkv_decode_rect", lib().pkv_decode_rect(
         _dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
         _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
-        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d, S, tile_tokens,
+        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d, ids_ptr, n, S, tile_tokens,
         float(sm_scale), _dev(out, torch.float16, "out"), _dev(ws, torch.uint8, "ws"), ws.numel(),
         _stream(stream)))
+
+
+def pkv_decode_buckets(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
+                       seq_lens: torch.Tensor, host_seq_lens, bucket_tokens: int, params: PlanParams,
+                       sm_scale: float, out: torch.Tensor, ws: torch.Tensor, *, stream=None) -> int:
+    """Length-bucket route; returns the number of kernel launches issued."""
+    B, Hq, d = q.shape
+    num_pages, _, Hkv, _ = k_cache.shape
+    lens, lens_ptr = _host_i32(host_seq_lens)
+    launches = ctypes.c_int32(0)
+    _check("pkv_decode_buckets", lib().pkv_decode_buckets(
+        _dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
+        _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
+        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), lens_ptr, B, Hq, Hkv, d,
+        int(bucket_tokens), ctypes.byref(params), float(sm_scale), _dev(out, torch.float16, "out"),
+        _dev(ws, torch.uint8, "ws"), ws.numel(), _stream(stream), ctypes.byref(launches)))
+    return int(launches.value)
 
 
 def pkv_check_device_status(ws: torch.Tensor, stream=None) -> int:

@@ -3,8 +3,11 @@
 // leaves the stream untouched.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
+#include <utility>
+#include <vector>
 #include <cstdint>
 #include <cstring>
 
@@ -167,15 +170,22 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
 
 int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
                     const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
-                    int32_t Hq, int32_t Hkv, int32_t d, int32_t S, int32_t tile_tokens, float sm_scale,
-                    uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+                    int32_t Hq, int32_t Hkv, int32_t d, const int32_t* row_ids, int32_t n_rows, int32_t S,
+                    int32_t tile_tokens, float sm_scale, uint16_t* out, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
   int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
   if (st != PKV_OK) return st;
   int G = 0;
   if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
   if (S < 1 || !std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
   if (tile_tokens <= 0 || tile_tokens % kPageSize != 0) return PKV_ERR_UNSUPPORTED;
-  const int32_t slots = pkv_max_tasks(B, Hkv, S);
+  if (row_ids) {
+    if (n_rows < 1 || n_rows > kMaxRectRows) return PKV_ERR_INVALID_ARG;
+    for (int j = 0; j < n_rows; ++j)
+      if (row_ids[j] < 0 || row_ids[j] >= B) return PKV_ERR_INVALID_ARG;
+  }
+  const int32_t rows = row_ids ? n_rows : B;
+  const int32_t slots = pkv_max_tasks(rows, Hkv, S);
   if (slots < 0) return PKV_ERR_INVALID_ARG;
   if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, slots)) return PKV_ERR_WORKSPACE;
   if ((int64_t)slots * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
@@ -184,7 +194,66 @@ int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
   a.S = S;
   a.tile_tokens = tile_tokens;
   a.max_tasks = slots;
+  a.n_rows = row_ids ? n_rows : 0;
+  for (int j = 0; j < a.n_rows; ++j) a.row_ids[j] = row_ids[j];
   return from_hip(launch_decode(a, G, 2, slots, stream));
+}
+
+int pkv_decode_buckets(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                       const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens,
+                       const int32_t* host_seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                       int32_t bucket_tokens, const pkv_plan_params* params, float sm_scale, uint16_t* out,
+                       void* ws, size_t ws_bytes, hipStream_t stream, int32_t* launches) {
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
+  if (st != PKV_OK) return st;
+  int G = 0;
+  if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
+  if (!host_seq_lens || !params || bucket_tokens < 0 || !std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
+  const pkv_plan_params p = *params;
+  if (p.page_size != kPageSize || p.tile_tokens <= 0 || p.tile_tokens % kPageSize != 0) return PKV_ERR_UNSUPPORTED;
+  if (p.num_kv_heads != Hkv || p.split_min < 1 || p.split_min > p.split_max || p.target_tasks < 1)
+    return PKV_ERR_INVALID_ARG;
+  // group rows by route length (exact length, or ceil(length / bucket_tokens)); empty
+  // rows form their own group so that their output is written as zeros
+  std::vector<std::pair<int64_t, int32_t>> keyed(B);
+  for (int32_t i = 0; i < B; ++i) {
+    const int32_t n = host_seq_lens[i];
+    if (n < 0) return PKV_ERR_INVALID_ARG;
+    const int64_t key = n == 0 ? -1 : (bucket_tokens == 0 ? n : (n + bucket_tokens - 1) / bucket_tokens);
+    keyed[i] = {key, i};
+  }
+  std::stable_sort(keyed.begin(), keyed.end(),
+                   [](const std::pair<int64_t, int32_t>& x, const std::pair<int64_t, int32_t>& y) {
+                     return x.first < y.first;
+                   });
+  struct Bucket {
+    int32_t first, count, S;
+  };
+  std::vector<Bucket> buckets;
+  int64_t need = 0;
+  for (int32_t b = 0; b < B;) {
+    int32_t e = b;
+    while (e < B && keyed[e].first == keyed[b].first && e - b < kMaxRectRows) ++e;
+    const int32_t nb = e - b;
+    int64_t S = (p.target_tasks + (int64_t)nb * Hkv - 1) / ((int64_t)nb * Hkv);
+    S = std::min<int64_t>(std::max<int64_t>(S, p.split_min), p.split_max);
+    buckets.push_back({b, nb, (int32_t)S});
+    need = std::max<int64_t>(need, (int64_t)nb * Hkv * S);
+    b = e;
+  }
+  if (need > INT32_MAX || ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, (int32_t)need)) return PKV_ERR_WORKSPACE;
+  if (need * (int64_t)slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  int32_t count = 0;
+  for (const Bucket& bk : buckets) {  // one rectangular split launch + one merge launch per bucket
+    int32_t ids[kMaxRectRows];
+    for (int32_t j = 0; j < bk.count; ++j) ids[j] = keyed[bk.first + j].second;
+    st = pkv_decode_rect(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq, Hkv, d,
+                         ids, bk.count, bk.S, p.tile_tokens, sm_scale, out, ws, ws_bytes, stream);
+    if (st != PKV_OK) return st;
+    count += 2;
+  }
+  if (launches) *launches = count;
+  return PKV_OK;
 }
 
 int pkv_check_device_status(void* ws, hipStream_t stream, uint32_t* error_bits) {

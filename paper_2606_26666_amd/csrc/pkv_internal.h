@@ -13,6 +13,7 @@ constexpr int kHeadDim = 128;
 constexpr int kPageSize = 16;
 constexpr int kMaxPlanBatch = 4096;
 constexpr int kMaxFusedPlanBatch = 1024;
+constexpr int kMaxRectRows = 64;  // rows a rectangular launch can name (kernel arguments)
 constexpr size_t kWsReadyOffset = 64;  // plan-ready flag inside the workspace header
 constexpr size_t kWsHeaderBytes = 256;
 
@@ -54,6 +55,8 @@ struct DecodeArgs {
   int32_t max_tasks;
   int32_t S;            // rectangular route only
   int32_t tile_tokens;  // rectangular route only
+  int32_t n_rows;       // rectangular route: rows named in row_ids (0: rows 0..B-1)
+  int32_t row_ids[kMaxRectRows];
   float scale_log2;     // sm_scale * log2(e)
   // planning inside the decode launch (pkv_plan_decode)
   PlanArgs plan;

@@ -863,14 +863,17 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   }
 }
 
-// Rectangular grid: workgroup (i, s, g) in slot order (i*S + s)*Hkv + g.
+// Rectangular grid: workgroup (j, s, g) in slot order (j*S + s)*Hkv + g, where j
+// indexes the launch's rows: row_ids[j] when the launch names its rows (a length
+// bucket; Q and out are then read and written by index), else row j.
 template <int G, int W>
 __global__ __launch_bounds__(W * 64) void rect_kernel(DecodeArgs a) {
   __shared__ float lds[lds_floats<G, W>()];
   const int slot = blockIdx.x;
   const int g = slot % a.Hkv;
   const int s = (slot / a.Hkv) % a.S;
-  const int row = slot / (a.Hkv * a.S);
+  const int j = slot / (a.Hkv * a.S);
+  const int row = a.n_rows > 0 ? a.row_ids[j] : j;
   int n = uniform(a.seq_lens[row]);
   if (n < 0 || n > a.max_pages_per_row * P) {
     if (threadIdx.x == 0 && s == 0 && g == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
@@ -898,11 +901,12 @@ constexpr int kMergeThreads = 256;
 template <int G, bool RECT>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
   __shared__ float lds[merge_lds_floats<G>()];
-  const int row = blockIdx.x / a.Hkv;
+  const int j = blockIdx.x / a.Hkv;  // the launch's row index
   const int g = blockIdx.x % a.Hkv;
+  const int row = (RECT && a.n_rows > 0) ? a.row_ids[j] : j;
   int slot0, nsplit;
   if (RECT) {
-    slot0 = row * a.S * a.Hkv + g;
+    slot0 = j * a.S * a.Hkv + g;
     nsplit = a.S;
   } else {
     const int off = a.split_offsets[row];
@@ -939,10 +943,11 @@ __global__ __launch_bounds__(256) void read_kernel(const uint4* __restrict__ src
 template <int G, int W>
 hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t s) {
   if (mode == 2) {
-    hipLaunchKernelGGL((rect_kernel<G, W>), dim3(a.B * a.Hkv * a.S), dim3(W * 64), 0, s, a);
+    const int rows = a.n_rows > 0 ? a.n_rows : a.B;
+    hipLaunchKernelGGL((rect_kernel<G, W>), dim3(rows * a.Hkv * a.S), dim3(W * 64), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((merge_kernel<G, true>), dim3(a.B * a.Hkv), dim3(kMergeThreads), 0, s, a);
+    hipLaunchKernelGGL((merge_kernel<G, true>), dim3(rows * a.Hkv), dim3(kMergeThreads), 0, s, a);
     return hipGetLastError();
   }
   if (mode == 1) {

@@ -85,12 +85,13 @@ def run_decode(case, bufs, fused=True, sm_scale=1.0, poison_ws=True):
     return out
 
 
-def run_rect(case, bufs, S, tile=32, sm_scale=1.0, poison_ws=True):
+def run_rect(case, bufs, S, tile=32, sm_scale=1.0, poison_ws=True, row_ids=None, out=None):
     if poison_ws:
         bufs.partial_region().fill_(0xFF)
-    out = torch.full((case.B, case.hq, case.d), float("nan"), dtype=torch.float16, device=DEV)
+    if out is None:
+        out = torch.full((case.B, case.hq, case.d), float("nan"), dtype=torch.float16, device=DEV)
     pkv.pkv_decode_rect(case.q_dev, case.k_dev, case.v_dev, case.bt_dev, case.lens_dev, S, tile, sm_scale,
-                        out, bufs.ws)
+                        out, bufs.ws, row_ids=row_ids)
     return out
 
 

@@ -23,7 +23,7 @@ def test_exports_every_header_function():
     names = pkv.header_functions()
     assert {"pkv_plan", "pkv_decode", "pkv_decode_rect", "pkv_max_tasks", "pkv_workspace_size",
             "pkv_workspace_init", "pkv_check_device_status", "pkv_status_string", "pkv_stream_copy", "pkv_stream_read",
-            "pkv_plan_decode"} <= set(names)
+            "pkv_plan_decode", "pkv_decode_buckets"} <= set(names)
     for n in names:
         assert hasattr(L, n), n
 
@@ -115,13 +115,18 @@ def test_rect_validation():
     def rect(**kw):
         a = dict(q=FAKE, S=16, tile=32, ws_bytes=1 << 22, B=2, d=128)
         a.update(kw)
-        return L.pkv_decode_rect(a["q"], FAKE, FAKE, 100, FAKE, 10, FAKE, a["B"], 32, 8, a["d"], a["S"],
+        ids = (ctypes.c_int32 * len(a.get("ids", []) or [0]))(*(a.get("ids") or [0]))
+        return L.pkv_decode_rect(a["q"], FAKE, FAKE, 100, FAKE, 10, FAKE, a["B"], 32, 8, a["d"],
+                                 ids if a.get("ids") is not None else None, a.get("n", 0), a["S"],
                                  a["tile"], 1.0, FAKE, FAKE, a["ws_bytes"], None)
     assert rect(S=0) == pkv.PKV_ERR_INVALID_ARG
     assert rect(tile=24) == pkv.PKV_ERR_UNSUPPORTED
     assert rect(d=96) == pkv.PKV_ERR_UNSUPPORTED
     assert rect(q=0) == pkv.PKV_ERR_INVALID_ARG
     assert rect(ws_bytes=2 * 8 * 16 * 2080) == pkv.PKV_ERR_WORKSPACE  # header missing
+    assert rect(ids=[0, 5], n=2) == pkv.PKV_ERR_INVALID_ARG              # row 5 outside B = 2
+    assert rect(ids=[0], n=65) == pkv.PKV_ERR_INVALID_ARG                # more than 64 rows
+    assert rect(ids=[1], n=1, S=0) == pkv.PKV_ERR_INVALID_ARG
 
 
 def test_copy_and_init_validation():

@@ -278,3 +278,39 @@ def test_plan_decode_benchmark_configs(name):
     assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), name)
     tasks, _ = read_plan(bufs)
     assert np.array_equal(tasks, oracle_plan(case, p)[0])
+
+
+def test_rect_named_rows_reads_and_writes_by_index():
+    case = Case(RAGGED, seed=14)
+    bufs = bufs_for(case, 16, rect_splits=16)
+    ids = [12, 0, 7]
+    out = run_rect(case, bufs, 16, row_ids=ids)
+    full = run_rect(case, bufs, 16)
+    others = [i for i in range(case.B) if i not in ids]
+    assert torch.equal(out[ids], full[ids])
+    assert torch.all(torch.isnan(out[others].float()))  # rows not named are untouched
+
+
+def test_exact_length_buckets_match_rectangular_grid():
+    case = Case(RAGGED, seed=15)   # every length distinct: one row per bucket, S = 64
+    p = plan_params(8, 16, 64, 512)
+    bufs = bufs_for(case, 64)
+    out = torch.full((case.B, case.hq, case.d), float("nan"), dtype=torch.float16, device="cuda")
+    launches = pkv.pkv_decode_buckets(case.q_dev, case.k_dev, case.v_dev, case.bt_dev, case.lens_dev, case.lens,
+                                      0, p, 1.0, out, bufs.ws)
+    assert launches == 2 * len(set(case.lens.tolist()))
+    assert torch.equal(out, run_rect(case, bufs, 64))
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), "exact buckets")
+
+
+def test_coarse_buckets_on_benchmark_config():
+    case, w = Case.from_workload("b8_bimodal")
+    p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks)
+    bufs = bufs_for(case, w.split_max)
+    out = torch.full((case.B, case.hq, case.d), float("nan"), dtype=torch.float16, device="cuda")
+    launches = pkv.pkv_decode_buckets(case.q_dev, case.k_dev, case.v_dev, case.bt_dev, case.lens_dev, case.lens,
+                                      16384, p, 1.0, out, bufs.ws)
+    groups = len({-(-int(n) // 16384) for n in case.lens})
+    assert launches == 2 * groups
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), "coarse buckets")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
