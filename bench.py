@@ -42,6 +42,8 @@ PROFILES = os.path.join(ROOT, "profiles")
 KV_BYTES_PER_TOKEN = 2 * 8 * 128 * 2   # K and V, Hkv=8, d=128, fp16
 SLOT_BYTES = 2080                      # fp32 m[4], l[4], acc[4][128]
 TASK_BYTES = 20
+BUCKET_TOKENS = 16384   # coarse-bucket width: rows grouped by ceil(len / 16384)
+ROUTES = ("plan+fused", "one-launch", "two-kernel", "exact-buckets", "coarse-buckets")
 
 
 def kernel_hash() -> str:
@@ -88,6 +90,8 @@ class Runner:
         self.policy = policy
         self.route = route
         self.fused = route != "two-kernel"
+        self.cur_lens = w.lengths_at(0)
+        self.last_launches = 0
         self.gen = torch.Generator(device=self.dev)
         self.gen.manual_seed(seed * 4 + 3)
         self.bt_host = w.block_table
@@ -117,17 +121,23 @@ class Runner:
             self.k[self.pages_steps[step], self.slots_steps[step]] = nk
             self.v[self.pages_steps[step], self.slots_steps[step]] = nv
         self.lens.copy_(self.lens_steps[step])
+        self.cur_lens = self.lens_host[step]
         return self.lens_host[step]
 
     def plan(self):
-        if self.route == "one-launch":
-            return  # the decode launch plans
+        if self.route in ("one-launch", "exact-buckets", "coarse-buckets"):
+            return  # the decode launch plans, or the bucket route plans on the host
         b = self.bufs
         self.pkv.pkv_plan(self.lens, None, self.w.num_pages, self.params, b.tasks, b.split_offsets, b.num_tasks,
                           b.ws, max_pages_per_row=self.w.max_pages_per_row)
 
     def decode(self):
         b = self.bufs
+        if self.route in ("exact-buckets", "coarse-buckets"):
+            self.last_launches = self.pkv.pkv_decode_buckets(
+                self.q, self.k, self.v, self.bt, self.lens, self.cur_lens,
+                0 if self.route == "exact-buckets" else BUCKET_TOKENS, self.params, 1.0, self.out, b.ws)
+            return
         if self.route == "one-launch":
             self.pkv.pkv_plan_decode(self.q, self.k, self.v, self.bt, self.lens, self.params, b.tasks,
                                      b.split_offsets, b.num_tasks, 1.0, self.out, b.ws)
@@ -232,8 +242,42 @@ def summarize(runner, m):
         "decode_gbs": achieved,
         "step_gbs": float(np.mean(alg)) / (float(np.mean(m["step_ms"])) / 1e3) / 1e9,
         "tasks_per_step": float(np.mean(m["ntasks"])),
-        "launches_per_step": {"one-launch": 1, "plan+fused": 2, "two-kernel": 3}[runner.route],
+        "launches_per_step": launches_per_step(runner),
+        **route_counters(runner, m),
     }
+
+
+def launches_per_step(runner):
+    if runner.route in ("exact-buckets", "coarse-buckets"):
+        return runner.last_launches
+    return {"one-launch": 1, "plan+fused": 2, "two-kernel": 3}[runner.route]
+
+
+def route_counters(runner, m):
+    """Scheduler-derived counters of the paper's Tab. 4 for the last timed step: split
+    workgroups per CU (256 CUs), useful KV MiB, partial-state (merge) MiB, merge launches."""
+    w = runner.w
+    lens = np.asarray(m["lens"][-1], dtype=np.int64)
+    T = w.tile_tokens
+    tiles = -(-lens // T)
+    p = runner.params
+    if runner.route in ("exact-buckets", "coarse-buckets"):
+        keys = [(-1 if n == 0 else (n if runner.route == "exact-buckets" else -(-n // BUCKET_TOKENS))) for n in lens]
+        wgs = 0
+        groups = 0
+        for k in sorted(set(keys)):
+            nb = keys.count(k)
+            for c in range(0, nb, 64):
+                n = min(64, nb - c)
+                S = min(max(-(-p.target_tasks // (n * w.hkv)), p.split_min), p.split_max)
+                wgs += n * w.hkv * S
+                groups += 1
+        slots, merge_launches = wgs, groups
+    else:
+        wgs = slots = m["ntasks"][-1]
+        merge_launches = 1 if runner.route == "two-kernel" else 0
+    return {"split_wg_per_cu": wgs / 256.0, "useful_kv_mib": float(lens.sum()) * KV_BYTES_PER_TOKEN / 2**20,
+            "merge_mib": slots * SLOT_BYTES / 2**20, "merge_launches": merge_launches}
 
 
 def read_traffic(workload):
@@ -291,9 +335,12 @@ def main():
     ap.add_argument("--policy", type=int, default=1,
                     help="split policy: 0 one split count from the active batch size, 1 tile quota (smallest "
                          "per-split tile quota whose task count fits --target-tasks)")
-    ap.add_argument("--route", default="plan+fused", choices=["plan+fused", "one-launch", "two-kernel"],
+    ap.add_argument("--route", default="plan+fused", choices=list(ROUTES),
                     help="plan+fused: planner kernel + fused split/merge kernel (2 launches); one-launch: "
-                         "planner inside the decode launch; two-kernel: planner, split kernel, merge kernel")
+                         "planner inside the decode launch; two-kernel: planner, split kernel, merge kernel; "
+                         "exact-buckets / coarse-buckets: host-grouped rows, a rectangular launch pair per group")
+    ap.add_argument("--routes-table", default="b8_bimodal",
+                    help="workload on which every route is also timed with its Tab. 4 counters ('none' to skip)")
     ap.add_argument("--no-flush", action="store_true", help="keep KV warm in the last-level cache")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -329,6 +376,15 @@ def main():
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
         del r
+    if args.routes_table != "none":
+        table = {}
+        for route in ROUTES:
+            r = Runner(args.routes_table, args.seed, args.target_tasks, 50, route=route, policy=args.policy)
+            res = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
+            table[route] = {k: res[k] for k in ("tok_s", "ms_per_step", "launches_per_step", "split_wg_per_cu",
+                                                "useful_kv_mib", "merge_mib", "merge_launches")}
+            del r
+        extra["routes_" + args.routes_table] = table
     traffic = read_traffic(args.workload)
     line = {
         "metric": METRIC,
