@@ -52,7 +52,6 @@ extern "C" {
 #define PKV_DEVERR_TASK 4u    /* a task outside the batch or its row's block table: skipped;
                                  outputs are unspecified unless the task list came from
                                  pkv_plan for the same seq_lens */
-#define PKV_DEVERR_PLAN_WAIT 8u /* pkv_plan_decode: a workgroup gave up waiting for the plan */
 
 /* pkv_decode flags. */
 #define PKV_FUSED_MERGE 1 /* merge in the split kernel by the last-arriving split (Sec. 3.4) */
@@ -102,8 +101,7 @@ typedef struct {
 int32_t pkv_max_tasks(int32_t B, int32_t Hkv, int32_t split_max);
 
 /* Bytes of workspace for batches of up to B rows and up to max_tasks partial-state
- * slots: a 256-byte header (error word, plan-ready flag), B*Hkv completion counters,
- * and max_tasks
+ * slots: a 256-byte header (error word), B*Hkv completion counters, and max_tasks
  * slots of fp32 {acc[G][d], m[G], l[G]} padded to 16 bytes (2080 bytes at G=4,
  * d=128). Returns 0 on a bad argument. The rectangular route needs
  * max_tasks >= B * Hkv * S. One workspace serves calls with one B: pkv_plan and
@@ -155,11 +153,13 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
                int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out, void* ws,
                size_t ws_bytes, hipStream_t stream);
 
-/* pkv_plan followed by pkv_decode with PKV_FUSED_MERGE, in one kernel launch: the
- * launch's first workgroup builds the task list (written to tasks, split_offsets and
- * num_tasks exactly as pkv_plan writes them) and the other workgroups start on it once
- * it is published. Arguments as for pkv_plan and pkv_decode; the block table is
+/* pkv_plan followed by pkv_decode with PKV_FUSED_MERGE, in one kernel launch: every
+ * workgroup runs the planner's arithmetic on seq_lens and takes its task from the
+ * result, and the first workgroup also writes tasks, split_offsets and num_tasks exactly
+ * as pkv_plan writes them. Arguments as for pkv_plan and pkv_decode; the block table is
  * checked by the decode (not by the planner), B <= 1024, params->num_kv_heads == Hkv.
+ * The completion counters must be zero at launch: pkv_workspace_init zeroes them and
+ * every completed pkv_plan, pkv_decode or pkv_plan_decode call leaves them zero.
  * Outputs are bit-identical to the two-call sequence. */
 int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
                     int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,

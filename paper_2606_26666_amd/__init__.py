@@ -5,7 +5,6 @@ behind the C ABI of include/pkv.h); this package is its Python binding.
 """
 from ._binding import (  # noqa: F401
     PKV_DEVERR_PAGE_ID,
-    PKV_DEVERR_PLAN_WAIT,
     PKV_DEVERR_SEQ_LEN,
     PKV_DEVERR_TASK,
     PKV_ERR_DEVICE,

@@ -25,7 +25,6 @@ PKV_ERR_DEVICE = 5
 PKV_DEVERR_SEQ_LEN = 1
 PKV_DEVERR_PAGE_ID = 2
 PKV_DEVERR_TASK = 4
-PKV_DEVERR_PLAN_WAIT = 8
 PKV_FUSED_MERGE = 1
 PKV_SPLIT_BATCH = 0
 PKV_SPLIT_QUOTA = 1

@@ -4,7 +4,6 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
-#include <atomic>
 #include <cmath>
 #include <utility>
 #include <vector>
@@ -107,9 +106,6 @@ int make_plan_args(const int32_t* seq_lens, const int32_t* block_table, int32_t 
   return PKV_OK;
 }
 
-// Unique per launch: the plan-ready flag of a fused plan + decode launch holds it.
-std::atomic<unsigned long long> g_launch_token{1};
-
 }  // namespace
 
 extern "C" {
@@ -164,7 +160,8 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
   a.split_offsets = split_offsets;
   a.num_tasks = num_tasks;
   a.max_tasks = max_tasks;
-  // one workgroup per possible task; those past *num_tasks exit at once
+  // grid: max_tasks, capped at the workgroups the device holds at once (each workgroup
+  // loops over tasks with the grid as stride)
   return from_hip(launch_decode(a, G, flags == PKV_FUSED_MERGE ? 1 : 0, max_tasks, stream));
 }
 
@@ -314,8 +311,6 @@ int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
   a.num_tasks = num_tasks;
   a.max_tasks = max_tasks;
   a.plan = pa;
-  a.ready = reinterpret_cast<unsigned long long*>(static_cast<char*>(ws) + kWsReadyOffset);
-  a.token = g_launch_token.fetch_add(1);
   return from_hip(launch_decode(a, G, 3, max_tasks, stream));
 }
 

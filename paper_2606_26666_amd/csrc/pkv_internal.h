@@ -14,7 +14,6 @@ constexpr int kPageSize = 16;
 constexpr int kMaxPlanBatch = 4096;
 constexpr int kMaxFusedPlanBatch = 1024;
 constexpr int kMaxRectRows = 64;  // rows a rectangular launch can name (kernel arguments)
-constexpr size_t kWsReadyOffset = 64;  // plan-ready flag inside the workspace header
 constexpr size_t kWsHeaderBytes = 256;
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -58,10 +57,7 @@ struct DecodeArgs {
   int32_t n_rows;       // rectangular route: rows named in row_ids (0: rows 0..B-1)
   int32_t row_ids[kMaxRectRows];
   float scale_log2;     // sm_scale * log2(e)
-  // planning inside the decode launch (pkv_plan_decode)
-  PlanArgs plan;
-  unsigned long long* ready;  // flag in the workspace header
-  unsigned long long token;   // unique per launch
+  PlanArgs plan;  // planning inside the decode launch (pkv_plan_decode)
 };
 
 

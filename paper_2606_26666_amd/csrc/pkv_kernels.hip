@@ -537,31 +537,53 @@ constexpr int lds_floats() {
 constexpr int kPlanThreads = 256;
 
 // inclusive prefix sum over the 64 lanes of a wave
-__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
+// Wave-wide scans on DPP: row shifts build prefixes inside each 16-lane row, the row
+// broadcasts 15 and 31 carry them across rows. Lanes without a source read 0, the
+// identity of the sums and of the max over non-negative values used here. The whole
+// wave must be active.
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ int dpp_i32(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, false);
+}
+
+template <typename Op>
+__device__ __forceinline__ int wave_scan_i32(int x, Op op) {
+  x = op(x, dpp_i32<0x111>(x));  // row_shr:1
+  x = op(x, dpp_i32<0x112>(x));  // row_shr:2
+  x = op(x, dpp_i32<0x114>(x));  // row_shr:4
+  x = op(x, dpp_i32<0x118>(x));  // row_shr:8
+  x = op(x, dpp_i32<0x142, 0xA>(x));  // row_bcast:15 into rows 1 and 3
+  x = op(x, dpp_i32<0x143, 0xC>(x));  // row_bcast:31 into rows 2 and 3
   return x;
 }
 
-__device__ __forceinline__ int wave_sum(int x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
-  return x;
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  return wave_scan_i32(x, [](int u, int v) { return u + v; });
+}
+
+__device__ __forceinline__ int wave_sum(int x) { return __builtin_amdgcn_readlane(wave_incl_scan(x), 63); }
+
+__device__ __forceinline__ int wave_max(int x) {  // x >= 0
+  return __builtin_amdgcn_readlane(wave_scan_i32(x, [](int u, int v) { return u > v ? u : v; }), 63);
+}
+
+template <int CTRL, int ROWS = 0xF>
+__device__ __forceinline__ long long dpp_i64(long long x) {
+  const int lo = dpp_i32<CTRL, ROWS>((int)x);
+  const int hi = dpp_i32<CTRL, ROWS>((int)(x >> 32));
+  return (long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
 }
 
 __device__ __forceinline__ long long wave_sum64(long long x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
-  return x;
-}
-
-__device__ __forceinline__ int wave_max(int x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x = max(x, __shfl_xor(x, off));
-  return x;
+  x += dpp_i64<0x111>(x);
+  x += dpp_i64<0x112>(x);
+  x += dpp_i64<0x114>(x);
+  x += dpp_i64<0x118>(x);
+  x += dpp_i64<0x142, 0xA>(x);
+  x += dpp_i64<0x143, 0xC>(x);
+  const unsigned lo = __builtin_amdgcn_readlane((int)x, 63);
+  const unsigned hi = __builtin_amdgcn_readlane((int)(x >> 32), 63);
+  return (long long)(((unsigned long long)hi << 32) | lo);
 }
 
 // Plan outputs read in the same kernel by other workgroups go out with agent-scope
@@ -585,8 +607,10 @@ struct PlanLds {
   int* wmax;       // [NT / 64]
 };
 
-template <int NT, bool COHERENT>
-__device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
+// Steps 1-3: validated lengths in L.len, split_offsets in L.off; returns the task count
+// (every thread). `report` selects the workgroup that raises device error bits.
+template <int NT>
+__device__ __forceinline__ int plan_compute(const PlanArgs& a, const PlanLds& L, bool report) {
   constexpr int NW = NT / 64;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -600,7 +624,7 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
   for (int i = r0; i < r0 + per && i < B; ++i) {
     int n = a.seq_lens[i];
     if (n < 0 || n > cap) {
-      atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
+      if (report) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
       n = 0;
     }
     L.len[i] = n;
@@ -614,7 +638,7 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
       if (jp < (L.len[i] + a.page_size - 1) / a.page_size) {
         const int phys = a.block_table[k];
         if (phys < 0 || phys >= a.num_pages) {
-          atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
+          if (report) atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
           L.len[i] = 0;  // benign race: every writer stores 0
         }
       }
@@ -651,48 +675,45 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
   }
   // policy 0: one split count S from the active batch size (Sec. 3.5);
   // policy 1: a tile quota Q per split from the batch's total work
-  long long S = 0, Q = 1;
+  int S = 0, Q = 1;
   if (a.policy == 0) {
     const long long denom = (long long)(active > 0 ? active : 1) * a.Hkv;
-    S = (a.target_tasks + denom - 1) / denom;
-    if (S < a.split_min) S = a.split_min;
-    if (S > a.split_max) S = a.split_max;
+    const long long s0 = (a.target_tasks + denom - 1) / denom;
+    S = (int)(s0 < a.split_min ? a.split_min : (s0 > a.split_max ? a.split_max : s0));
   } else {
     // smallest Q in [1, max_tiles] with Hkv * sum_i min(split_max, ceil(tiles_i / Q))
     // <= target_tasks (the count only falls as Q grows), else max_tiles. Bisection;
     // the upper end starts at ceil(total / (target/Hkv - active)) when that bounds it.
-    const long long per_head = a.target_tasks / a.Hkv;
-    long long hi = max(1, max_tiles);
-    if (per_head > active) hi = min(hi, max(1LL, (total_tiles + per_head - active - 1) / (per_head - active)));
-    long long lo = 1;
-    auto count_local = [&](long long q) {
-      long long c = 0;
-      for (int i = r0; i < r0 + per && i < B; ++i) {
-        const long long t = (L.len[i] + T - 1) / T;
-        c += min((long long)a.split_max, (t + q - 1) / q);
-      }
-      return c;
-    };
+    // Counts fit in 32 bits: B * split_max * Hkv is bounded by the task buffer's size.
+    const int per_head = a.target_tasks / a.Hkv;
+    int hi = max(1, max_tiles);
+    if (per_head > active)
+      hi = (int)min((long long)hi, max(1LL, (total_tiles + per_head - active - 1) / (per_head - active)));
+    int lo = 1;
+    auto nsplit_at = [&](int t, int q) { return t > 0 ? min(a.split_max, (t + q - 1) / q) : 0; };
     __syncthreads();  // every wave has read the batch sums in L.w64
-    if (B <= 64) {  // all rows live in wave 0: search without barriers
+    if (B <= 64) {  // one row per lane of wave 0: search without barriers
       if (wave == 0) {
+        const int t = lane < B ? (L.len[lane] + T - 1) / T : 0;
         while (lo < hi) {
-          const long long mid = (lo + hi) >> 1;
-          if (wave_sum64(count_local(mid)) <= per_head) hi = mid; else lo = mid + 1;
+          const int mid = (lo + hi) >> 1;
+          if (wave_sum(nsplit_at(t, mid)) <= per_head) hi = mid; else lo = mid + 1;
         }
-        if (lane == 0) L.w64[0] = lo;
+        if (lane == 0) L.wave[0] = lo;
       }
       __syncthreads();
-      Q = L.w64[0];
+      Q = L.wave[0];
     } else {
       int buf = 0;
       while (lo < hi) {
-        const long long mid = (lo + hi) >> 1;
-        const long long c = wave_sum64(count_local(mid));
-        long long* red = L.w64 + buf * NW;  // two buffers: one barrier per round
+        const int mid = (lo + hi) >> 1;
+        int c = 0;
+        for (int i = r0; i < r0 + per && i < B; ++i) c += nsplit_at((L.len[i] + T - 1) / T, mid);
+        c = wave_sum(c);
+        int* red = reinterpret_cast<int*>(L.w64) + buf * NW;  // two buffers: one barrier per round
         if (lane == 0) red[wave] = c;
         __syncthreads();
-        long long tot = 0;
+        int tot = 0;
 #pragma unroll
         for (int w = 0; w < NW; ++w) tot += red[w];
         if (tot <= per_head) hi = mid; else lo = mid + 1;
@@ -703,13 +724,13 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
   }
   auto row_nsplit = [&](int n) -> int {
     const int tiles = (n + T - 1) / T;
-    if (a.policy == 0) return (int)min((long long)tiles, S);
-    return (int)min((long long)a.split_max, (tiles + Q - 1) / Q);
+    if (a.policy == 0) return min(tiles, S);
+    return min(a.split_max, (tiles + Q - 1) / Q);
   };
   // 3. exclusive scan of nsplit over rows -> split_offsets
   int local = 0;
   for (int i = r0; i < r0 + per && i < B; ++i) local += row_nsplit(L.len[i]);
-  const int incl = wave_incl_scan(local, lane);
+  const int incl = wave_incl_scan(local);
   __syncthreads();  // every wave has read L.wave
   if (lane == 63) L.wave[wave] = incl;
   __syncthreads();
@@ -721,37 +742,61 @@ __device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
   }
   if (tid == NT - 1) L.off[B] = run;
   __syncthreads();
-  for (int i = tid; i <= B; i += NT) st_i32<COHERENT>(a.split_offsets + i, L.off[i]);
   long long ntasks = (long long)L.off[B] * a.Hkv;
   if (ntasks > a.max_tasks) {  // excluded by host validation; never write past the buffer
-    if (tid == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
+    if (report && tid == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
     ntasks = 0;
   }
-  if (tid == 0) st_i32<COHERENT>(a.num_tasks, (int)ntasks);
-  // 4. task k = (split_offsets[i] + s) * Hkv + g: balanced tile range s of row i
-  for (int k = tid; k < (int)ntasks; k += NT) {
-    const int sr = k / a.Hkv;
-    const int g = k % a.Hkv;
-    int lo = 0, hi = B;  // largest i with off[i] <= sr
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (L.off[mid] <= sr) lo = mid; else hi = mid;
-    }
-    const int i = lo;
-    const int sp = sr - L.off[i];
-    const int n = L.len[i];
-    const int tiles = (n + T - 1) / T;
-    const int ns = L.off[i + 1] - L.off[i];
-    const int b0 = (int)(((long long)sp * tiles) / ns);
-    const int b1 = (int)(((long long)(sp + 1) * tiles) / ns);
-    int* t = reinterpret_cast<int*>(a.tasks + k);
-    st_i32<COHERENT>(t + 0, i);
-    st_i32<COHERENT>(t + 1, g);
-    st_i32<COHERENT>(t + 2, sp);
-    st_i32<COHERENT>(t + 3, b0 * T);
-    st_i32<COHERENT>(t + 4, min(b1 * T, n));
+  return (int)ntasks;
+}
+
+// Step 4: task k = (split_offsets[i] + s) * Hkv + g covers the balanced tile range s of
+// row i: [floor(s*tiles/nsplit), floor((s+1)*tiles/nsplit)) tiles.
+struct TaskRec {
+  int row, g, split, t0, t1;
+};
+
+__device__ __forceinline__ TaskRec plan_task(const PlanArgs& a, const PlanLds& L, int k) {
+  const int sr = k / a.Hkv;
+  int lo = 0, hi = a.B;  // largest i with off[i] <= sr
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (L.off[mid] <= sr) lo = mid; else hi = mid;
   }
-  for (int k = tid; k < B * a.Hkv; k += NT) st_i32<COHERENT>(a.counters + k, 0);
+  const int T = a.tile_tokens;
+  const int sp = sr - L.off[lo];
+  const int n = L.len[lo];
+  const int tiles = (n + T - 1) / T;
+  const int ns = L.off[lo + 1] - L.off[lo];
+  const int b0 = (int)(((long long)sp * tiles) / ns);
+  const int b1 = (int)(((long long)(sp + 1) * tiles) / ns);
+  return TaskRec{lo, k % a.Hkv, sp, b0 * T, min(b1 * T, n)};
+}
+
+// The planner's outputs: split_offsets, num_tasks, the task list and zeroed completion
+// counters.
+template <int NT, bool COHERENT>
+__device__ __forceinline__ void plan_write(const PlanArgs& a, const PlanLds& L, int ntasks, bool zero_counters) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i <= a.B; i += NT) st_i32<COHERENT>(a.split_offsets + i, L.off[i]);
+  if (tid == 0) st_i32<COHERENT>(a.num_tasks, ntasks);
+  for (int k = tid; k < ntasks; k += NT) {
+    const TaskRec r = plan_task(a, L, k);
+    int* t = reinterpret_cast<int*>(a.tasks + k);
+    st_i32<COHERENT>(t + 0, r.row);
+    st_i32<COHERENT>(t + 1, r.g);
+    st_i32<COHERENT>(t + 2, r.split);
+    st_i32<COHERENT>(t + 3, r.t0);
+    st_i32<COHERENT>(t + 4, r.t1);
+  }
+  if (zero_counters)
+    for (int k = tid; k < a.B * a.Hkv; k += NT) st_i32<COHERENT>(a.counters + k, 0);
+}
+
+template <int NT, bool COHERENT>
+__device__ __forceinline__ void plan_body(const PlanArgs& a, const PlanLds& L) {
+  const int ntasks = plan_compute<NT>(a, L, true);
+  plan_write<NT, COHERENT>(a, L, ntasks, true);
 }
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
@@ -765,11 +810,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
 
 // Workqueue split kernel. FUSED: the last split of each (row, KV head) to finish merges
 // all of that pair's splits in split order (Sec. 3.4, atomic completion counter).
-// PLAN: workgroup 0 first builds the task list (the planner above) and publishes it
-// through a flag holding this launch's token; the other workgroups wait for the token.
-// Workgroup 0 is dispatched first and never waits, so the wait always ends; a bounded
-// spin turns a missing token into an error instead of a hang.
-constexpr int kSpinLimit = 1 << 24;
+// PLAN: the planner runs inside the launch (see below).
 
 template <int G, int W, bool FUSED, bool PLAN>
 __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
@@ -781,46 +822,38 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   __shared__ int p_wave[W];
   __shared__ long long p_w64[2 * W];
   __shared__ int p_wmax[W];
+  // PLAN: every workgroup runs the planner's arithmetic on seq_lens and takes its tasks
+  // from the result; workgroup 0 also writes the task list. The completion counters are
+  // zero at launch (pkv_workspace_init sets them, every completed launch restores them).
+  const PlanLds PL{p_len, p_off, p_wave, p_w64, p_wmax};
+  int plan_ntasks = 0;
   if (PLAN) {
-    if (blockIdx.x == 0) {
-      plan_body<W * 64, true>(a.plan, PlanLds{p_len, p_off, p_wave, p_w64, p_wmax});
-      __builtin_amdgcn_s_waitcnt(0);  // every plan store acknowledged
-      __syncthreads();
-      if (threadIdx.x == 0) __hip_atomic_store(a.ready, a.token, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    } else {
-      if (threadIdx.x == 0) {
-        int spins = 0;
-        while (__hip_atomic_load(a.ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != a.token &&
-               ++spins < kSpinLimit)
-          __builtin_amdgcn_s_sleep(2);
-        lds_last = spins < kSpinLimit;
-        if (!lds_last) atomicOr(a.err, (unsigned)PKV_DEVERR_PLAN_WAIT);
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-      }
-      __syncthreads();
-      if (!lds_last) return;
-    }
+    plan_ntasks = plan_compute<W * 64>(a.plan, PL, blockIdx.x == 0);
+    if (blockIdx.x == 0) plan_write<W * 64, false>(a.plan, PL, plan_ntasks, false);
   }
   // The first task record is fetched together with the task count (the grid never
   // exceeds max_tasks, so the record lies inside the task buffer even when unused).
   int rec[4];
-  {
-    const int* tp = reinterpret_cast<const int*>(a.tasks + blockIdx.x);
-    rec[0] = ld_i32<PLAN>(tp + 0);
-    rec[1] = ld_i32<PLAN>(tp + 1);
-    rec[2] = ld_i32<PLAN>(tp + 3);
-    rec[3] = ld_i32<PLAN>(tp + 4);
-  }
-  int ntasks = uniform(ld_i32<PLAN>(a.num_tasks));
+  auto fetch = [&](int t) {
+    if (PLAN) {
+      const TaskRec r = plan_task(a.plan, PL, t);
+      rec[0] = r.row;
+      rec[1] = r.g;
+      rec[2] = r.t0;
+      rec[3] = r.t1;
+    } else {
+      const int* tp = reinterpret_cast<const int*>(a.tasks + t);
+      rec[0] = tp[0];
+      rec[1] = tp[1];
+      rec[2] = tp[3];
+      rec[3] = tp[4];
+    }
+  };
+  if (!PLAN || (int)blockIdx.x < plan_ntasks) fetch(blockIdx.x);  // PLAN: only real tasks
+  int ntasks = PLAN ? plan_ntasks : uniform(*a.num_tasks);
   if (ntasks > a.max_tasks) ntasks = a.max_tasks;
   for (int t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    if (t != (int)blockIdx.x) {
-      const int* tp = reinterpret_cast<const int*>(a.tasks + t);
-      rec[0] = ld_i32<PLAN>(tp + 0);
-      rec[1] = ld_i32<PLAN>(tp + 1);
-      rec[2] = ld_i32<PLAN>(tp + 3);
-      rec[3] = ld_i32<PLAN>(tp + 4);
-    }
+    if (t != (int)blockIdx.x) fetch(t);
     const int row = uniform(rec[0]), g = uniform(rec[1]);
     const int t0 = uniform(rec[2]), t1 = uniform(rec[3]);
     if (row < 0 || row >= a.B || g < 0 || g >= a.Hkv || t0 < 0 || t1 <= t0 ||
@@ -830,8 +863,8 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
     }
     run_task<G, W, FUSED>(a, row, g, t0, t1, t, lds);
     if (FUSED) {
-      const int off = uniform(ld_i32<PLAN>(a.split_offsets + row));
-      int nsplit = uniform(ld_i32<PLAN>(a.split_offsets + row + 1)) - off;
+      const int off = uniform(PLAN ? PL.off[row] : a.split_offsets[row]);
+      int nsplit = uniform(PLAN ? PL.off[row + 1] : a.split_offsets[row + 1]) - off;
       if (off < 0 || nsplit < 1 || (long long)(off + nsplit) * a.Hkv > a.max_tasks) {
         if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
         nsplit = 0;  // never reached by the counter: no merge from inconsistent offsets
@@ -858,8 +891,10 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
     __syncthreads();
   }
   if (FUSED) {  // rows without tasks: their output is zero
-    for (int i = blockIdx.x; i < a.B; i += gridDim.x)
-      if (ld_i32<PLAN>(a.split_offsets + i + 1) == ld_i32<PLAN>(a.split_offsets + i)) zero_row<G>(a, i);
+    for (int i = blockIdx.x; i < a.B; i += gridDim.x) {
+      const bool empty = PLAN ? PL.off[i + 1] == PL.off[i] : a.split_offsets[i + 1] == a.split_offsets[i];
+      if (empty) zero_row<G>(a, i);
+    }
   }
 }
 
@@ -940,6 +975,20 @@ __global__ __launch_bounds__(256) void read_kernel(const uint4* __restrict__ src
   if (x == 0x9E3779B9u) *sink = x;  // keeps the loads; practically never taken
 }
 
+// Workgroups of `kernel` resident on the current device at once (occupancy x CUs),
+// at least one per CU. The split kernels loop over tasks with the grid as stride, so
+// their grid is the task bound capped at this count (taken once per kernel, on the
+// first device that launches it).
+int resident_blocks(const void* kernel, int threads) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    cus = 256;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess || per_cu < 1)
+    per_cu = 1;
+  return per_cu * cus;
+}
+
 template <int G, int W>
 hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t s) {
   if (mode == 2) {
@@ -951,13 +1000,19 @@ hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t 
     return hipGetLastError();
   }
   if (mode == 1) {
+    static const int resident = resident_blocks((const void*)split_kernel<G, W, true, false>, W * 64);
+    grid = grid < resident ? grid : resident;
     hipLaunchKernelGGL((split_kernel<G, W, true, false>), dim3(grid), dim3(W * 64), 0, s, a);
     return hipGetLastError();
   }
   if (mode == 3) {
+    static const int resident = resident_blocks((const void*)split_kernel<G, W, true, true>, W * 64);
+    grid = grid < resident ? grid : resident;
     hipLaunchKernelGGL((split_kernel<G, W, true, true>), dim3(grid), dim3(W * 64), 0, s, a);
     return hipGetLastError();
   }
+  static const int resident = resident_blocks((const void*)split_kernel<G, W, false, false>, W * 64);
+  grid = grid < resident ? grid : resident;
   hipLaunchKernelGGL((split_kernel<G, W, false, false>), dim3(grid), dim3(W * 64), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
