@@ -1,25 +1,29 @@
 #!/usr/bin/env python
 """Decode throughput of the paged GQA decode path on one MI355X.
 
-One step is one decode step of the whole path for every active row: the planner kernel
-(compact workqueue) and the fused split-attention + last-arriver merge kernel, over a
-native paged KV cache (Hq=32, Hkv=8, d=128, fp16, page 16). Before each step, outside
-the timed region, the step's new token K/V is written into the pool, seq_lens grows by
-one, and a 1 GiB streaming read evicts the 256 MB last-level cache (MALL) so that KV is
-read from HBM as it would be with the other layers' KV in between. The eviction reads
-only, so no dirty lines are left to be written back during the timed step.
+One step is one decode step of the whole path for every active row: the compact
+workqueue planner and the split-attention kernel with its last-arriver merge, over a
+native paged KV cache (Hq=32, Hkv=8, d=128, fp16, page 16). The default route runs all
+of it in one launch (every workgroup derives its tasks from the lengths); --route picks
+the planner-kernel + fused-kernel pair, the three-launch ablation or the length-bucket
+routes. Before each step, outside the timed region, the step's new token K/V is written
+into the pool, seq_lens grows by one, and a 1 GiB streaming read evicts the 256 MB
+last-level cache (MALL) so that KV is read from HBM as it would be with the other
+layers' KV in between. The eviction reads only, so no dirty lines are left to be
+written back during the timed step.
 
-Timing: HIP events on the stream the kernels run on, around each step (plan + decode)
-and around the decode kernel alone. Steps are enqueued back to back behind the cache
-eviction copy, so the events measure device time, not Python launch latency; a second,
-host-synchronized pass gives wall time per step.
+Timing: HIP events on the stream the kernels run on, around each step. Steps are
+enqueued back to back behind the cache eviction read, so the events measure device
+time, not Python launch latency; a second pass with an event between planner and
+decode launches gives the per-kernel split, and a host-synchronized pass gives wall
+time per step.
 
 value = decode tokens / second = sum of active rows over the timed steps / sum of step
-times (event intervals around plan + decode, marker latency included). roofline.achieved
-= algorithmic bytes of one decode-kernel launch / its average duration (event interval
-around the launch less the median empty-interval latency measured in the same run; it
-agrees with rocprofv3's kernel duration). cpu_baseline = the fp64 numpy oracle on the
-host over the same steps.
+times (event intervals around the step, marker latency included). roofline.achieved =
+algorithmic bytes of one decode-kernel launch / its average duration (event interval
+around the launch, which agrees with rocprofv3's kernel duration to about 1%). extra.beta_read_gbs is the streaming-read
+bandwidth of the 1 GiB eviction read in the same run (the calibration probe beta).
+cpu_baseline = the fp64 numpy oracle on the host over the same steps' inputs.
 """
 from __future__ import annotations
 
@@ -217,15 +221,49 @@ def measure(runner, steps, warmup, flush_bufs):
                 marker_ms=marker_ms)
 
 
+def calibrate(pkv, torch, flush_bufs, reps=10, launches=200):
+    """Device constants of the cost model, measured in this run: beta = streaming-read
+    bandwidth of a 1 GiB read (GB/s), lambda = device time per back-to-back launch of a
+    near-empty kernel (us), from events around `launches` 16-byte reads queued behind
+    a backlog of large reads."""
+    Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    buf, sink = flush_bufs if flush_bufs is not None else (
+        torch.zeros(1 << 30, dtype=torch.uint8, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"))
+    pkv.pkv_stream_read(buf, sink)
+    ms = []
+    for _ in range(reps):
+        e0, e1 = Ev(), Ev()
+        e0.record()
+        pkv.pkv_stream_read(buf, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    beta = buf.numel() / (float(np.median(ms)) / 1e3) / 1e9
+    # launch gap: queue enough 1 GiB reads ahead that the host has enqueued every
+    # small launch before the device reaches them, so the interval is device time
+    small = buf[:16]
+    for _ in range(max(4, launches // 16)):
+        pkv.pkv_stream_read(buf, sink)
+    e0, e1 = Ev(), Ev()
+    e0.record()
+    for _ in range(launches):
+        pkv.pkv_stream_read(small, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    lam = e0.elapsed_time(e1) * 1e3 / launches
+    return {"beta_read_gbs": beta, "launch_gap_us": lam}
+
+
 def summarize(runner, m):
     w = runner.w
     tokens = w.batch * len(m["step_ms"])
     step_s = sum(m["step_ms"]) / 1e3
     alg, kv = zip(*(algorithmic_bytes(l, t, w.hq, w.head_dim) for l, t in zip(m["lens"], m["ntasks"])))
     marker = float(np.median(m["marker_ms"]))
-    # decode-kernel duration: events around the launch, less the latency of an empty
-    # event interval (the event markers' own cost, measured in the same run)
-    dec_ms = float(np.mean(m["dec_ms"])) - marker
+    # decode-kernel duration: the event interval around the launch (within ~1% of
+    # rocprofv3's kernel duration; an empty interval's marker latency is reported
+    # beside it but does not add to a busy interval)
+    dec_ms = float(np.mean(m["dec_ms"]))
     achieved = float(alg[-1]) / (dec_ms / 1e3) / 1e9  # the breakdown pass ran the last step's inputs
     return {
         "tok_s": tokens / step_s,
@@ -299,11 +337,15 @@ def read_traffic(workload):
         return None
 
 
-def cpu_baseline(runner, steps, budget_s=20.0):
-    """The fp64 oracle on the host over the same steps' inputs (bounded to ~budget_s)."""
-    from threadpoolctl import threadpool_info
+def cpu_baseline(runner, steps, budget_s=15.0):
+    """The fp64 oracle on the host over the same steps' inputs (bounded to ~budget_s),
+    with the BLAS pool at its default size; then one step on one thread, and the tiny
+    512-token case, both reported beside it."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import ref_decode
+    from workloads import make_workload
+    from workloads.values import host_normal_f16, q_values
     w = runner.w
     k = runner.k.cpu().numpy()
     v = runner.v.cpu().numpy()
@@ -318,9 +360,23 @@ def cpu_baseline(runner, steps, budget_s=20.0):
             break
     dt = time.perf_counter() - t0
     threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
+    with threadpool_limits(1):
+        t1 = time.perf_counter()
+        ref_decode(q, k, v, w.block_table, w.lengths_at(0))
+        dt1 = time.perf_counter() - t1
+    tw = make_workload("tiny")
+    rng = np.random.Generator(np.random.PCG64(11))
+    shape = (tw.num_pages, tw.page_size, tw.hkv, tw.head_dim)
+    tk, tv = host_normal_f16(shape, rng), host_normal_f16(shape, rng)
+    tq = q_values(tw.batch, tw.hq, tw.head_dim, rng)
+    t2 = time.perf_counter()
+    ref_decode(tq, tk, tv, tw.block_table, tw.lengths_at(0))
+    dt_tiny = time.perf_counter() - t2
     return {"value": done * w.batch / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{w.name}: {done} decode steps (of {steps}) of the fp64 numpy oracle, "
-                      f"{dt:.1f} s, BLAS threads {threads}, host CPUs {len(os.sched_getaffinity(0))}"}
+                      f"{dt:.1f} s, BLAS threads {threads}, host CPUs {len(os.sched_getaffinity(0))}",
+            "one_thread_value": w.batch / dt1,
+            "tiny_step_ms": dt_tiny * 1e3}
 
 
 def main():
@@ -335,7 +391,7 @@ def main():
     ap.add_argument("--policy", type=int, default=1,
                     help="split policy: 0 one split count from the active batch size, 1 tile quota (smallest "
                          "per-split tile quota whose task count fits --target-tasks)")
-    ap.add_argument("--route", default="plan+fused", choices=list(ROUTES),
+    ap.add_argument("--route", default="one-launch", choices=list(ROUTES),
                     help="plan+fused: planner kernel + fused split/merge kernel (2 launches); one-launch: "
                          "planner inside the decode launch; two-kernel: planner, split kernel, merge kernel; "
                          "exact-buckets / coarse-buckets: host-grouped rows, a rectangular launch pair per group")
@@ -366,12 +422,13 @@ def main():
         flush_bufs = (torch.zeros(1 << 30, dtype=torch.uint8, device="cuda"),
                       torch.zeros(1, dtype=torch.int32, device="cuda"))
 
+    cal = calibrate(pkv, torch, flush_bufs)
     steps_cfg = max(args.steps, 20 if args.workload == "b1" else 50)
     main_run = Runner(args.workload, args.seed, args.target_tasks, steps_cfg, route=args.route,
                       policy=args.policy)
     m = measure(main_run, args.steps, args.warmup, flush_bufs)
     s = summarize(main_run, m)
-    extra = {args.workload: s}
+    extra = {args.workload: s, "calibration": cal}
     for name in [x for x in args.also.split(",") if x and x != "none" and x != args.workload]:
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))

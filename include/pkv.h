@@ -82,7 +82,7 @@ typedef struct {
  *   tile_tokens  split granularity in tokens (the paper's 32-token tile, Sec. 3.2);
  *                a positive multiple of page_size
  *   num_kv_heads Hkv
- *   split_min, split_max  split-count bounds, 1 <= split_min <= split_max
+ *   split_min, split_max  split-count bounds, 1 <= split_min <= split_max <= 65536
  *   target_tasks desired task count, >= 1 (see the policies above)
  *   policy       PKV_SPLIT_BATCH or PKV_SPLIT_QUOTA
  * Split s of row i owns tiles [floor(s*tiles_i/nsplit_i), floor((s+1)*tiles_i/nsplit_i)). */
@@ -174,7 +174,8 @@ int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
  * neutral state (-inf, 0, 0) and exits before loading Q (Sec. 3.3). The launch covers
  * rows 0..B-1 when row_ids is NULL, else the n_rows (1..64) rows listed in the HOST
  * array row_ids, reading Q and writing out by index (indexed Q/O, Sec. 4.6). With the
- * same S the output is bit-identical to pkv_decode. ws needs max_tasks >= rows * Hkv * S;
+ * same S the output is bit-identical to pkv_decode. 1 <= S <= 65536. ws needs
+ * max_tasks >= rows * Hkv * S;
  * tile_tokens as in pkv_plan_params. */
 int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
                     int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,

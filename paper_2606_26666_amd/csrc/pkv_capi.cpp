@@ -75,7 +75,8 @@ int make_plan_args(const int32_t* seq_lens, const int32_t* block_table, int32_t 
   const pkv_plan_params p = *params;
   if (p.page_size != kPageSize) return PKV_ERR_UNSUPPORTED;
   if (p.tile_tokens <= 0 || p.tile_tokens % p.page_size != 0) return PKV_ERR_UNSUPPORTED;
-  if (p.num_kv_heads < 1 || p.split_min < 1 || p.split_min > p.split_max || p.target_tasks < 1)
+  if (p.num_kv_heads < 1 || p.split_min < 1 || p.split_min > p.split_max || p.split_max > kMaxSplits ||
+      p.target_tasks < 1)
     return PKV_ERR_INVALID_ARG;
   if (p.policy != PKV_SPLIT_BATCH && p.policy != PKV_SPLIT_QUOTA) return PKV_ERR_INVALID_ARG;
   if ((int64_t)max_pages_per_row * p.page_size > INT32_MAX) return PKV_ERR_INVALID_ARG;
@@ -174,7 +175,7 @@ int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
   if (st != PKV_OK) return st;
   int G = 0;
   if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
-  if (S < 1 || !std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
+  if (S < 1 || S > kMaxSplits || !std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
   if (tile_tokens <= 0 || tile_tokens % kPageSize != 0) return PKV_ERR_UNSUPPORTED;
   if (row_ids) {
     if (n_rows < 1 || n_rows > kMaxRectRows) return PKV_ERR_INVALID_ARG;

@@ -13,6 +13,7 @@ constexpr int kHeadDim = 128;
 constexpr int kPageSize = 16;
 constexpr int kMaxPlanBatch = 4096;
 constexpr int kMaxFusedPlanBatch = 1024;
+constexpr int kMaxSplits = 65536;  // split_max and the rectangular S: keeps split bounds in 32 bits
 constexpr int kMaxRectRows = 64;  // rows a rectangular launch can name (kernel arguments)
 constexpr size_t kWsHeaderBytes = 256;
 

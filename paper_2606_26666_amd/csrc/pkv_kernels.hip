@@ -87,6 +87,14 @@ constexpr float kNegInf = -__builtin_inff();
 // exponentiated with exp2. l < 0 marks a split that met an invalid page.
 template <int G> constexpr int slot_floats() { return G * D + ((2 * G + 3) / 4) * 4; }
 
+// Split s of a row with `tiles` tiles cut into ns splits starts at tile
+// floor(s * tiles / ns). With tiles = q * ns + r this is s * q + floor(s * r / ns), and
+// s * r < 2^32 for ns <= kMaxSplits, so no 64-bit division is needed.
+__device__ __forceinline__ int split_bound(int s, int tiles, int ns) {
+  const unsigned q = (unsigned)tiles / (unsigned)ns, r = (unsigned)tiles % (unsigned)ns;
+  return (int)((unsigned)s * q + ((unsigned)s * r) / (unsigned)ns);
+}
+
 // Slots are accessed through one raw buffer descriptor over the whole slot array. When
 // another workgroup merges them inside the same kernel they use agent-scope (sc1)
 // accesses, which on gfx950 are coherent across the per-XCD L2 caches, so a completed
@@ -123,13 +131,17 @@ __device__ __forceinline__ void st_state4(__amdgpu_buffer_rsrc_t r, int off, v4f
 // the thread count. Every merge in the library goes through merge_group, so all routes
 // round identically. A (row, KV head) with a marked split (l < 0) is zeroed.
 //
-// Latency: for up to kMergeBlock splits, a thread's acc loads (one run of one float4
-// column) and the m/l loads are in flight together, so the merge costs about one
-// memory round trip.
+// Latency: for up to kMergeBlock splits, a thread's m/l loads and then its acc loads
+// (one run of one float4 column) are in flight together, so the merge costs about one
+// memory round trip. The loads are straight-line code: a state that does not exist
+// is read at an offset past the end of the slot buffer, which a buffer load returns
+// as zero without touching memory, and its weight is zero. Loads then retire in issue
+// order, so the weights are computed while the acc loads are still arriving.
 constexpr int kMergeBlock = 64;  // split states staged in LDS at a time
 constexpr int kMergeRun = 32;    // splits per run
 constexpr int kRunsPerBlock = kMergeBlock / kMergeRun;
 constexpr int kMaxMergeWaves = 16;
+constexpr int kOutOfRange = (int)0x80000000u;  // buffer offset past any slot buffer
 
 template <int G>
 constexpr int merge_lds_floats() {
@@ -166,13 +178,11 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
       const int e = tid + k * NT;
-      if (e < cnt * G) {
-        mv[k] = ld_state<COHERENT>(pr, soff(s0 + e / G) + (G * D + myh) * 4);
-        lv[k] = ld_state<COHERENT>(pr, soff(s0 + e / G) + (G * D + G + myh) * 4);
-      } else {
-        mv[k] = kNegInf;
-        lv[k] = 0.0f;
-      }
+      const bool ok = e < cnt * G;
+      const int off = ok ? soff(s0 + e / G) + (G * D + myh) * 4 : kOutOfRange;
+      const float m = ld_state<COHERENT>(pr, off);
+      lv[k] = ld_state<COHERENT>(pr, off + G * 4);  // l sits G floats after m (0 when absent)
+      mv[k] = ok ? m : kNegInf;
     }
   };
   // max and marker over this thread's states, then over lanes of the same head, then
@@ -226,48 +236,48 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     const int cnt = min(kMergeBlock, nsplit - s0);
     const int nrun = (cnt + kMergeRun - 1) / kMergeRun;
     const int nitems = E4 * nrun;
-    auto issue_item = [&](int it) {
+    auto issue_item = [&](int it) {  // it >= nitems: every load is out of range (zeros)
       const int e4 = it % E4;
       const int sb = (it / E4) * kMergeRun;
       const int n = min(kMergeRun, cnt - sb);
 #pragma unroll
       for (int u = 0; u < kMergeRun; ++u)
-        if (u < n) v[u] = ld_state4<COHERENT>(pr, soff(s0 + sb + u) + e4 * 16);
+        v[u] = ld_state4<COHERENT>(pr, u < n ? soff(s0 + sb + u) + e4 * 16 : kOutOfRange);
     };
     auto finish_item = [&](int it) {
       const int e4 = it % E4;
       const int run = it / E4;
       const int sb = run * kMergeRun;
-      const int n = min(kMergeRun, cnt - sb);
       const int h = (e4 * 4) / D;
       v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
       float lacc = 0.0f;
       const bool first_col = (e4 * 4) % D == 0;
+      // entries past the block's states have weight 0 and zero data: adding 0 * 0 to a
+      // sum that starts at +0 leaves it unchanged, so no per-split branch is needed
 #pragma unroll
       for (int u = 0; u < kMergeRun; ++u) {
-        if (u < n) {
-          const float w = lw[(sb + u) * G + h];
-          acc.x = __builtin_fmaf(w, v[u].x, acc.x);
-          acc.y = __builtin_fmaf(w, v[u].y, acc.y);
-          acc.z = __builtin_fmaf(w, v[u].z, acc.z);
-          acc.w = __builtin_fmaf(w, v[u].w, acc.w);
-          if (first_col) lacc = __builtin_fmaf(w, ll[(sb + u) * G + h], lacc);
-        }
+        const float w = lw[(sb + u) * G + h];
+        acc.x = __builtin_fmaf(w, v[u].x, acc.x);
+        acc.y = __builtin_fmaf(w, v[u].y, acc.y);
+        acc.z = __builtin_fmaf(w, v[u].z, acc.z);
+        acc.w = __builtin_fmaf(w, v[u].w, acc.w);
+        lacc = __builtin_fmaf(w, ll[(sb + u) * G + h], lacc);
       }
       *reinterpret_cast<v4f*>(part + run * G * D + e4 * 4) = acc;
       if (first_col) partL[run * G + h] = lacc;
     };
     __syncthreads();  // the previous block's LDS is consumed
-    if (tid < nitems) issue_item(tid);  // in flight while m and l arrive
     load_ml(s0, cnt);
+    issue_item(tid);  // in flight while the weights are formed
     if (one_block) reduce_max();
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
       const int e = tid + k * NT;
-      if (e < cnt * G) {
+      if (e < kMergeBlock * G) {
         const float M = sM[myh];
-        lw[e] = ex2(mv[k] - (M == kNegInf ? 0.0f : M));
-        ll[e] = lv[k];
+        const bool ok = e < cnt * G;
+        lw[e] = ok ? ex2(mv[k] - (M == kNegInf ? 0.0f : M)) : 0.0f;
+        ll[e] = ok ? lv[k] : 0.0f;
       }
     }
     __syncthreads();
@@ -607,10 +617,67 @@ struct PlanLds {
   int* wmax;       // [NT / 64]
 };
 
+// Steps 1-3 for a batch of at most 64 rows and no block-table check: lane i of wave 0
+// holds row i, every batch quantity is a wave reduction and split_offsets a wave scan,
+// so the workgroup meets a single barrier. Same results as the general path below.
+__device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanLds& L, bool report) {
+  const int lane = threadIdx.x & 63;
+  const int B = a.B;
+  const int T = a.tile_tokens;
+  const int cap = a.max_pages_per_row * a.page_size;
+  int n = lane < B ? a.seq_lens[lane] : 0;
+  if (n < 0 || n > cap) {
+    if (report) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
+    n = 0;
+  }
+  const int tiles = n > 0 ? (n - 1) / T + 1 : 0;
+  const int active = __popcll(__ballot(tiles > 0));
+  int nsplit;
+  if (a.policy == 0) {
+    const long long denom = (long long)(active > 0 ? active : 1) * a.Hkv;
+    const long long s0 = (a.target_tasks + denom - 1) / denom;
+    const int S = (int)(s0 < a.split_min ? a.split_min : (s0 > a.split_max ? a.split_max : s0));
+    nsplit = min(tiles, S);
+  } else {
+    // the quota search of the general path, one row per lane
+    const int per_head = a.target_tasks / a.Hkv;
+    const int max_tiles = wave_max(tiles);
+    int hi = max(1, max_tiles);
+    if (per_head > active) {
+      const long long total = wave_sum64(tiles);
+      const long long room = per_head - active;
+      if (total < (long long)hi * room) hi = (int)max(1LL, (total + room - 1) / room);
+    }
+    int lo = 1;
+    auto nsplit_at = [&](int q) { return tiles > 0 ? min(a.split_max, (tiles - 1) / q + 1) : 0; };
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (wave_sum(nsplit_at(mid)) <= per_head) hi = mid; else lo = mid + 1;
+    }
+    nsplit = nsplit_at(lo);
+  }
+  const int incl = wave_incl_scan(nsplit);
+  if (lane < B) {
+    L.len[lane] = n;
+    L.off[lane + 1] = incl;
+  }
+  if (lane == 0) L.off[0] = 0;
+}
+
 // Steps 1-3: validated lengths in L.len, split_offsets in L.off; returns the task count
 // (every thread). `report` selects the workgroup that raises device error bits.
 template <int NT>
 __device__ __forceinline__ int plan_compute(const PlanArgs& a, const PlanLds& L, bool report) {
+  if (a.B <= 64 && !a.block_table) {
+    if (threadIdx.x < 64) plan_compute_wave(a, L, report);
+    __syncthreads();
+    long long nt = (long long)L.off[a.B] * a.Hkv;
+    if (nt > a.max_tasks) {  // excluded by host validation; never write past the buffer
+      if (report && threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
+      nt = 0;
+    }
+    return (int)nt;
+  }
   constexpr int NW = NT / 64;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -768,8 +835,8 @@ __device__ __forceinline__ TaskRec plan_task(const PlanArgs& a, const PlanLds& L
   const int n = L.len[lo];
   const int tiles = (n + T - 1) / T;
   const int ns = L.off[lo + 1] - L.off[lo];
-  const int b0 = (int)(((long long)sp * tiles) / ns);
-  const int b1 = (int)(((long long)(sp + 1) * tiles) / ns);
+  const int b0 = split_bound(sp, tiles, ns);
+  const int b1 = split_bound(sp + 1, tiles, ns);
   return TaskRec{lo, k % a.Hkv, sp, b0 * T, min(b1 * T, n)};
 }
 
@@ -921,8 +988,8 @@ __global__ __launch_bounds__(W * 64) void rect_kernel(DecodeArgs a) {
     write_neutral<G>(a, slot);
     return;
   }
-  const int b0 = (int)(((long long)s * tiles) / ns);
-  const int b1 = (int)(((long long)(s + 1) * tiles) / ns);
+  const int b0 = split_bound(s, tiles, ns);
+  const int b1 = split_bound(s + 1, tiles, ns);
   const int t0 = b0 * T;
   const int t1 = min(b1 * T, n);
   run_task<G, W, false>(a, row, g, t0, t1, slot, lds);

@@ -76,6 +76,7 @@ def test_plan_validation():
     assert plan(L, params=b.PlanParams(16, 32, 0, 16, 64, 512)) == pkv.PKV_ERR_INVALID_ARG
     assert plan(L, params=b.PlanParams(16, 32, 8, 16, 64, 0)) == pkv.PKV_ERR_INVALID_ARG
     assert plan(L, params=b.PlanParams(16, 32, 8, 16, 64, 512, 2)) == pkv.PKV_ERR_INVALID_ARG  # policy
+    assert plan(L, params=b.PlanParams(16, 32, 1, 16, 65537, 512)) == pkv.PKV_ERR_INVALID_ARG  # split cap
     assert plan(L, max_tasks=2 * 8 * 64 - 1) == pkv.PKV_ERR_WORKSPACE
     assert plan(L, ws_bytes=511) == pkv.PKV_ERR_WORKSPACE
     assert plan(L, maxp=1 << 28) == pkv.PKV_ERR_INVALID_ARG
@@ -120,6 +121,7 @@ def test_rect_validation():
                                  ids if a.get("ids") is not None else None, a.get("n", 0), a["S"],
                                  a["tile"], 1.0, FAKE, FAKE, a["ws_bytes"], None)
     assert rect(S=0) == pkv.PKV_ERR_INVALID_ARG
+    assert rect(S=65537) == pkv.PKV_ERR_INVALID_ARG
     assert rect(tile=24) == pkv.PKV_ERR_UNSUPPORTED
     assert rect(d=96) == pkv.PKV_ERR_UNSUPPORTED
     assert rect(q=0) == pkv.PKV_ERR_INVALID_ARG

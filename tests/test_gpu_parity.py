@@ -60,6 +60,26 @@ def test_plan_bit_exact_random_batches(seed, policy):
     assert np.array_equal(tasks, rt) and np.array_equal(offs, ro)
 
 
+@pytest.mark.parametrize("policy", [0, 1])
+@pytest.mark.parametrize("B", [1, 2, 7, 33, 63, 64])
+def test_plan_bit_exact_small_batches(B, policy):
+    """Batches of up to 64 rows take the planner's one-wave path (no block-table check)."""
+    r = np.random.Generator(np.random.PCG64(300 + B + 1000 * policy))
+    lens = r.integers(0, 40000, size=B).astype(np.int32)
+    lens[r.random(B) < 0.25] = 0
+    if B == 33:
+        lens[:] = 0   # nothing active
+    case = Case(lens, hkv=8, hq=32, seed=B, rho=0.0, values=False)
+    for smin, smax, target in [(16, 64, 512), (1, 1, 512), (2, 9, 37), (1, 300, 100000)]:
+        p = plan_params(8, smin, smax, target, policy=policy)
+        bufs = bufs_for(case, smax)
+        run_plan(case, bufs, p)
+        tasks, offs = read_plan(bufs)
+        rt, ro, _ = oracle_plan(case, p)
+        assert np.array_equal(tasks, rt) and np.array_equal(offs, ro), (smin, smax, target)
+        assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
 @pytest.mark.parametrize("fused", [True, False])
 @pytest.mark.parametrize("hq,hkv", [(32, 8), (8, 8), (16, 8), (32, 4)])
 def test_decode_ragged_matches_oracle(fused, hq, hkv):
