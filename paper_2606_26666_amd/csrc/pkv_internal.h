@@ -56,9 +56,9 @@ struct DecodeArgs {
   int32_t S;            // rectangular route only
   int32_t tile_tokens;  // rectangular route only
   int32_t n_rows;       // rectangular route: rows named in row_ids (0: rows 0..B-1)
-  int32_t row_ids[kMaxRectRows];
   float scale_log2;     // sm_scale * log2(e)
-  PlanArgs plan;  // planning inside the decode launch (pkv_plan_decode)
+  PlanArgs plan;        // planning inside the decode launch (pkv_plan_decode)
+  int32_t row_ids[kMaxRectRows];  // last: only the rectangular route reads it
 };
 
 

@@ -617,6 +617,8 @@ struct PlanLds {
   int* wmax;       // [NT / 64]
 };
 
+constexpr int kCandidateRows = 16;  // batches up to this size search the quota 64-wide
+
 // Steps 1-3 for a batch of at most 64 rows and no block-table check: lane i of wave 0
 // holds row i, every batch quantity is a wave reduction and split_offsets a wave scan,
 // so the workgroup meets a single barrier. Same results as the general path below.
@@ -634,27 +636,54 @@ __device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanL
   const int active = __popcll(__ballot(tiles > 0));
   int nsplit;
   if (a.policy == 0) {
-    const long long denom = (long long)(active > 0 ? active : 1) * a.Hkv;
-    const long long s0 = (a.target_tasks + denom - 1) / denom;
-    const int S = (int)(s0 < a.split_min ? a.split_min : (s0 > a.split_max ? a.split_max : s0));
+    // 32-bit: denom <= B * Hkv and target + denom - 1 < 2^32
+    const unsigned denom = (unsigned)(active > 0 ? active : 1) * (unsigned)a.Hkv;
+    const int s0 = (int)(((unsigned)a.target_tasks + denom - 1u) / denom);
+    const int S = s0 < a.split_min ? a.split_min : (s0 > a.split_max ? a.split_max : s0);
     nsplit = min(tiles, S);
   } else {
-    // the quota search of the general path, one row per lane
+    // the quota search of the general path; same result, found in fewer steps
     const int per_head = a.target_tasks / a.Hkv;
     const int max_tiles = wave_max(tiles);
     int hi = max(1, max_tiles);
     if (per_head > active) {
-      const long long total = wave_sum64(tiles);
-      const long long room = per_head - active;
-      if (total < (long long)hi * room) hi = (int)max(1LL, (total + room - 1) / room);
+      const unsigned room = (unsigned)(per_head - active);
+      if (max_tiles < (1 << 25)) {  // the total fits in 31 bits
+        const unsigned total = (unsigned)wave_sum(tiles);
+        if ((unsigned long long)total < (unsigned long long)hi * room) hi = max(1u, (total + room - 1u) / room);
+      } else {
+        const long long total = wave_sum64(tiles);
+        if (total < (long long)hi * room) hi = (int)max(1LL, (total + room - 1) / (long long)room);
+      }
     }
+    auto nsplit_of = [&](int t, int q) { return t > 0 ? min(a.split_max, (t - 1) / q + 1) : 0; };
     int lo = 1;
-    auto nsplit_at = [&](int q) { return tiles > 0 ? min(a.split_max, (tiles - 1) / q + 1) : 0; };
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (wave_sum(nsplit_at(mid)) <= per_head) hi = mid; else lo = mid + 1;
+    if (B <= kCandidateRows) {
+      // 64-way search: lane j tests the quota lo + (j + 1) * step - 1 over every row; the
+      // first fitting candidate narrows [lo, hi] to one step (the count only falls as the
+      // quota grows)
+      while (lo < hi) {
+        const int step = (hi - lo + 64) >> 6;
+        const int q = min(hi, lo + (lane + 1) * step - 1);
+        int c = 0;
+        for (int i = 0; i < B; ++i) c += nsplit_of(__builtin_amdgcn_readlane(tiles, i), q);
+        const unsigned long long fit = __ballot(c <= per_head);
+        if (fit == 0) {  // nothing up to hi fits: one split per row
+          lo = hi;
+          break;
+        }
+        const int j = __ffsll((unsigned long long)fit) - 1;
+        const int qj = min(hi, lo + (j + 1) * step - 1);
+        if (j > 0) lo = min(hi, lo + j * step - 1) + 1;
+        hi = qj;
+      }
+    } else {
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (wave_sum(nsplit_of(tiles, mid)) <= per_head) hi = mid; else lo = mid + 1;
+      }
     }
-    nsplit = nsplit_at(lo);
+    nsplit = nsplit_of(tiles, lo);
   }
   const int incl = wave_incl_scan(nsplit);
   if (lane < B) {
@@ -893,6 +922,10 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   // from the result; workgroup 0 also writes the task list. The completion counters are
   // zero at launch (pkv_workspace_init sets them, every completed launch restores them).
   const PlanLds PL{p_len, p_off, p_wave, p_w64, p_wmax};
+  // Bring the argument block's pointer lines and the grid size into the scalar cache at
+  // the start, so later scalar loads of them do not wait on memory (after the planner,
+  // and at the end of the last task).
+  asm volatile("" ::"s"(a.q), "s"(a.partials), "s"(gridDim.x));
   int plan_ntasks = 0;
   if (PLAN) {
     plan_ntasks = plan_compute<W * 64>(a.plan, PL, blockIdx.x == 0);
