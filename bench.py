@@ -387,7 +387,8 @@ def main():
     ap.add_argument("--workload", default="b1")
     ap.add_argument("--also", default="b8_bimodal", help="comma-separated extra workloads, or 'none'")
     ap.add_argument("--seed", type=int, default=20260623)
-    ap.add_argument("--target-tasks", type=int, default=512)
+    ap.add_argument("--target-tasks", type=int, default=256,
+                    help="planner task target; 256 = one task per compute unit")
     ap.add_argument("--policy", type=int, default=1,
                     help="split policy: 0 one split count from the active batch size, 1 tile quota (smallest "
                          "per-split tile quota whose task count fits --target-tasks)")

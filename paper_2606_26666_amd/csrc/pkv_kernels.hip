@@ -665,8 +665,24 @@ __device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanL
       while (lo < hi) {
         const int step = (hi - lo + 64) >> 6;
         const int q = min(hi, lo + (lane + 1) * step - 1);
+        const float rq = __builtin_amdgcn_rcpf((float)q);
         int c = 0;
-        for (int i = 0; i < B; ++i) c += nsplit_of(__builtin_amdgcn_readlane(tiles, i), q);
+        for (int i = 0; i < B; ++i) {
+          const int t = __builtin_amdgcn_readlane(tiles, i);
+          if (t <= 0) continue;
+          // ceil(t / q) = floor((t - 1) / q) + 1. Below 2^22 the float quotient is within
+          // one of the exact one (operand exact, reciprocal and product each within
+          // 2^-23 relative), so one integer correction step makes it exact.
+          int f;
+          if (t <= (1 << 22)) {
+            f = (int)((float)(t - 1) * rq);
+            const int rem = (t - 1) - f * q;
+            f += (rem >= q) - (rem < 0);
+          } else {
+            f = (t - 1) / q;
+          }
+          c += min(a.split_max, f + 1);
+        }
         const unsigned long long fit = __ballot(c <= per_head);
         if (fit == 0) {  // nothing up to hi fits: one split per row
           lo = hi;

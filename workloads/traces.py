@@ -114,7 +114,7 @@ class Workload:
 
 
 def _build(name, lens, steps, rho, seed, rng_pages, num_pages=None, split=(16, 64),
-           target_tasks=512, append=True):
+           target_tasks=256, append=True):
     lens = np.asarray(lens, dtype=np.int64)
     reserved = lens + (steps if append else 0)
     bt, universe = page_table(reserved, PAGE, rho, rng_pages, num_pages=num_pages)
@@ -124,7 +124,7 @@ def _build(name, lens, steps, rho, seed, rng_pages, num_pages=None, split=(16, 6
 
 
 def make_workload(name: str, seed: int = 20260622, steps: int | None = None,
-                  target_tasks: int = 512) -> Workload:
+                  target_tasks: int = 256) -> Workload:
     """The benchmark configurations, as concrete seeded inputs.
 
     tiny        : B=1, 512 tokens (no append), pool of 64 pages, one split
