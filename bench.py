@@ -14,14 +14,15 @@ written back during the timed step.
 
 Timing: HIP events on the stream the kernels run on, around each step. Steps are
 enqueued back to back behind the cache eviction read, so the events measure device
-time, not Python launch latency; a second pass with an event between planner and
-decode launches gives the per-kernel split, and a host-synchronized pass gives wall
-time per step.
+time (launch overhead included), not Python launch latency; a second pass times the
+planner launch with events around it and the decode kernel with events stamped by its
+own launch, and a host-synchronized pass gives wall time per step.
 
 value = decode tokens / second = sum of active rows over the timed steps / sum of step
 times (event intervals around the step, marker latency included). roofline.achieved =
-algorithmic bytes of one decode-kernel launch / its average duration (event interval
-around the launch, which agrees with rocprofv3's kernel duration to about 1%). extra.beta_read_gbs is the streaming-read
+algorithmic bytes of one decode-kernel launch / its average execution time (start and
+stop events stamped by the launch itself, hipExtLaunchKernel, so the interval is the
+kernel's own, as rocprofv3 reports it). extra.beta_read_gbs is the streaming-read
 bandwidth of the 1 GiB eviction read in the same run (the calibration probe beta).
 cpu_baseline = the fp64 numpy oracle on the host over the same steps' inputs.
 """
@@ -47,7 +48,7 @@ KV_BYTES_PER_TOKEN = 2 * 8 * 128 * 2   # K and V, Hkv=8, d=128, fp16
 SLOT_BYTES = 2080                      # fp32 m[4], l[4], acc[4][128]
 TASK_BYTES = 20
 BUCKET_TOKENS = 16384   # coarse-bucket width: rows grouped by ceil(len / 16384)
-ROUTES = ("plan+fused", "one-launch", "two-kernel", "exact-buckets", "coarse-buckets")
+ROUTES = ("plan+fused", "one-launch", "two-kernel", "rect", "exact-buckets", "coarse-buckets")
 
 
 def kernel_hash() -> str:
@@ -100,6 +101,13 @@ class Runner:
         self.gen.manual_seed(seed * 4 + 3)
         self.bt_host = w.block_table
 
+    def rect_splits(self):
+        """Split count of the rectangular grid: the batch rule of the planner's policy 0,
+        S = clamp(ceil(target / (B_active * Hkv)), split_min, split_max), on the host."""
+        p, w = self.params, self.w
+        active = max(1, int(np.count_nonzero(np.asarray(self.cur_lens) > 0)))
+        return int(min(max(-(-p.target_tasks // (active * w.hkv)), p.split_min), p.split_max))
+
     def host_lengths(self, step):
         return self.w.lengths_at(step)
 
@@ -129,14 +137,20 @@ class Runner:
         return self.lens_host[step]
 
     def plan(self):
-        if self.route in ("one-launch", "exact-buckets", "coarse-buckets"):
-            return  # the decode launch plans, or the bucket route plans on the host
+        if self.route in ("one-launch", "rect", "exact-buckets", "coarse-buckets"):
+            return  # the decode launch plans, or the route's split count comes from the host
         b = self.bufs
         self.pkv.pkv_plan(self.lens, None, self.w.num_pages, self.params, b.tasks, b.split_offsets, b.num_tasks,
                           b.ws, max_pages_per_row=self.w.max_pages_per_row)
 
-    def decode(self):
+    def decode(self, events=None):
+        """events: (start, stop) stamped with the decode kernels' execution interval
+        (one-launch, plan+fused and two-kernel routes); None for a plain launch."""
         b = self.bufs
+        if self.route == "rect":
+            self.pkv.pkv_decode_rect(self.q, self.k, self.v, self.bt, self.lens, self.rect_splits(),
+                                     self.w.tile_tokens, 1.0, self.out, b.ws)
+            return
         if self.route in ("exact-buckets", "coarse-buckets"):
             self.last_launches = self.pkv.pkv_decode_buckets(
                 self.q, self.k, self.v, self.bt, self.lens, self.cur_lens,
@@ -144,10 +158,10 @@ class Runner:
             return
         if self.route == "one-launch":
             self.pkv.pkv_plan_decode(self.q, self.k, self.v, self.bt, self.lens, self.params, b.tasks,
-                                     b.split_offsets, b.num_tasks, 1.0, self.out, b.ws)
+                                     b.split_offsets, b.num_tasks, 1.0, self.out, b.ws, events=events)
             return
         self.pkv.pkv_decode(self.q, self.k, self.v, self.bt, self.lens, b.tasks, b.split_offsets, b.num_tasks,
-                            1.0, self.out, b.ws, fused=self.fused)
+                            1.0, self.out, b.ws, fused=self.fused, events=events)
 
 
 def measure(runner, steps, warmup, flush_bufs):
@@ -176,28 +190,36 @@ def measure(runner, steps, warmup, flush_bufs):
         runner.decode()
         e2.record()
         ev.append((e0, e2))
-        ntasks.append(runner.bufs.num_tasks.clone())
+        ntasks.append(runner.bufs.num_tasks.clone() if runner.route in ("one-launch", "plan+fused", "two-kernel")
+                      else route_slots(runner, runner.cur_lens)[0])
     torch.cuda.synchronize()
     step_ms = [a.elapsed_time(c) for a, c in ev]
-    ntasks = [int(t.item()) for t in ntasks]
+    ntasks = [int(t.item()) if hasattr(t, "item") else int(t) for t in ntasks]
     bits = pkv.pkv_check_device_status(runner.bufs.ws)
     if bits:
         raise RuntimeError(f"device error bits {bits}")
-    # per-kernel breakdown on the last step's inputs: events around each launch alone
-    # (kept out of the step timing above, since every event adds its own marker latency)
+    # per-kernel breakdown on the last step's inputs (kept out of the step timing above):
+    # events around the planner launch, and the decode kernels' own execution interval
+    # (stamped by the launch itself, the interval rocprofv3 reports); the bucket routes,
+    # several launches, take plain events around the decode call
+    kernel_stamps = runner.route in ("one-launch", "plan+fused", "two-kernel")
     ev = []
     for s in range(steps):
         flush()
-        e0, e1, e2 = Ev(), Ev(), Ev()
+        e0, e1, e2, e3 = Ev(), Ev(), Ev(), Ev()
         e0.record()
         runner.plan()
         e1.record()
-        runner.decode()
-        e2.record()
-        ev.append((e0, e1, e2))
+        if kernel_stamps:
+            runner.decode(events=(e2, e3))
+        else:
+            e2.record()
+            runner.decode()
+            e3.record()
+        ev.append((e0, e1, e2, e3))
     torch.cuda.synchronize()
-    plan_ms = [a.elapsed_time(b) for a, b, c in ev]
-    dec_ms = [b.elapsed_time(c) for a, b, c in ev]
+    plan_ms = [a.elapsed_time(b) for a, b, c, d in ev]
+    dec_ms = [c.elapsed_time(d) for a, b, c, d in ev]
     # marker latency alone: two events with nothing between them
     ev = []
     for s in range(steps):
@@ -260,16 +282,14 @@ def summarize(runner, m):
     step_s = sum(m["step_ms"]) / 1e3
     alg, kv = zip(*(algorithmic_bytes(l, t, w.hq, w.head_dim) for l, t in zip(m["lens"], m["ntasks"])))
     marker = float(np.median(m["marker_ms"]))
-    # decode-kernel duration: the event interval around the launch (within ~1% of
-    # rocprofv3's kernel duration; an empty interval's marker latency is reported
-    # beside it but does not add to a busy interval)
+    # decode-kernel duration: its execution interval as stamped by the launch (the
+    # duration rocprofv3 reports); the empty-interval marker latency is reported beside it
     dec_ms = float(np.mean(m["dec_ms"]))
     achieved = float(alg[-1]) / (dec_ms / 1e3) / 1e9  # the breakdown pass ran the last step's inputs
     return {
         "tok_s": tokens / step_s,
         "ms_per_step": float(np.mean(m["step_ms"])),
         "plan_ms": float(np.mean(m["plan_ms"])),
-        "decode_event_ms": float(np.mean(m["dec_ms"])),
         "event_marker_ms": marker,
         "decode_ms": dec_ms,
         "wall_ms_per_step": float(np.median(m["wall_ms"])),
@@ -288,7 +308,26 @@ def summarize(runner, m):
 def launches_per_step(runner):
     if runner.route in ("exact-buckets", "coarse-buckets"):
         return runner.last_launches
-    return {"one-launch": 1, "plan+fused": 2, "two-kernel": 3}[runner.route]
+    return {"one-launch": 1, "plan+fused": 2, "two-kernel": 3, "rect": 2}[runner.route]
+
+
+def route_slots(runner, lens):
+    """(split workgroups = partial-state slots, merge launches) of the host-planned routes
+    for one step's lengths: the rectangular grid and the length buckets."""
+    w, p = runner.w, runner.params
+    lens = np.asarray(lens, dtype=np.int64)
+    if runner.route == "rect":
+        return len(lens) * w.hkv * runner.rect_splits(), 1
+    keys = [(-1 if n == 0 else (n if runner.route == "exact-buckets" else -(-n // BUCKET_TOKENS))) for n in lens]
+    wgs = groups = 0
+    for k in sorted(set(keys)):
+        nb = keys.count(k)
+        for c in range(0, nb, 64):
+            n = min(64, nb - c)
+            S = min(max(-(-p.target_tasks // (n * w.hkv)), p.split_min), p.split_max)
+            wgs += n * w.hkv * S
+            groups += 1
+    return wgs, groups
 
 
 def route_counters(runner, m):
@@ -296,21 +335,9 @@ def route_counters(runner, m):
     workgroups per CU (256 CUs), useful KV MiB, partial-state (merge) MiB, merge launches."""
     w = runner.w
     lens = np.asarray(m["lens"][-1], dtype=np.int64)
-    T = w.tile_tokens
-    tiles = -(-lens // T)
-    p = runner.params
-    if runner.route in ("exact-buckets", "coarse-buckets"):
-        keys = [(-1 if n == 0 else (n if runner.route == "exact-buckets" else -(-n // BUCKET_TOKENS))) for n in lens]
-        wgs = 0
-        groups = 0
-        for k in sorted(set(keys)):
-            nb = keys.count(k)
-            for c in range(0, nb, 64):
-                n = min(64, nb - c)
-                S = min(max(-(-p.target_tasks // (n * w.hkv)), p.split_min), p.split_max)
-                wgs += n * w.hkv * S
-                groups += 1
-        slots, merge_launches = wgs, groups
+    if runner.route in ("rect", "exact-buckets", "coarse-buckets"):
+        wgs, merge_launches = route_slots(runner, lens)
+        slots = wgs
     else:
         wgs = slots = m["ntasks"][-1]
         merge_launches = 1 if runner.route == "two-kernel" else 0
@@ -395,9 +422,11 @@ def main():
     ap.add_argument("--route", default="one-launch", choices=list(ROUTES),
                     help="plan+fused: planner kernel + fused split/merge kernel (2 launches); one-launch: "
                          "planner inside the decode launch; two-kernel: planner, split kernel, merge kernel; "
+                         "rect: rectangular (B, Hkv, S) grid + merge kernel; "
                          "exact-buckets / coarse-buckets: host-grouped rows, a rectangular launch pair per group")
     ap.add_argument("--routes-table", default="b8_bimodal",
-                    help="workload on which every route is also timed with its Tab. 4 counters ('none' to skip)")
+                    help="comma-separated workloads on which every route is also timed with its Tab. 4 counters "
+                         "('none' to skip)")
     ap.add_argument("--no-flush", action="store_true", help="keep KV warm in the last-level cache")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -434,15 +463,15 @@ def main():
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
         del r
-    if args.routes_table != "none":
+    for wl in [x for x in args.routes_table.split(",") if x and x != "none"]:
         table = {}
         for route in ROUTES:
-            r = Runner(args.routes_table, args.seed, args.target_tasks, 50, route=route, policy=args.policy)
+            r = Runner(wl, args.seed, args.target_tasks, 50, route=route, policy=args.policy)
             res = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
             table[route] = {k: res[k] for k in ("tok_s", "ms_per_step", "launches_per_step", "split_wg_per_cu",
                                                 "useful_kv_mib", "merge_mib", "merge_launches")}
             del r
-        extra["routes_" + args.routes_table] = table
+        extra["routes_" + wl] = table
     traffic = read_traffic(args.workload)
     line = {
         "metric": METRIC,

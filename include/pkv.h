@@ -168,6 +168,26 @@ int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
                     int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* pkv_decode and pkv_plan_decode with kernel-execution timestamps, for measurement:
+ * start is recorded when the call's first kernel begins executing and stop when its
+ * last kernel has finished (the interval a profiler reports, without the queue's own
+ * packet latency). start and stop are events created by the caller (hipEventCreate, or
+ * a timing event that has been recorded once); either may be NULL. Results and errors
+ * as for the untimed calls. */
+int pkv_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                     int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                     const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                     const pkv_task* tasks, const int32_t* split_offsets, const int32_t* num_tasks,
+                     int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out, void* ws,
+                     size_t ws_bytes, hipStream_t stream, hipEvent_t start, hipEvent_t stop);
+int pkv_plan_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                          int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                          const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                          const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+                          int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
+                          void* ws, size_t ws_bytes, hipStream_t stream, hipEvent_t start,
+                          hipEvent_t stop);
+
 /* Rectangular split grid (Sec. 3.4): rows * Hkv * S split workgroups, then a merge over
  * all S columns (two kernels, no planner). Column s of a row owns the same balanced tile
  * range the planner gives split s when s < min(S, tiles); otherwise it writes the

@@ -55,6 +55,11 @@ _SIGS = {
                                   _F32, _I32, _P, _P, _SZ, _P]),
     "pkv_plan_decode": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
                                        ctypes.POINTER(PlanParams), _P, _I32, _P, _P, _F32, _P, _P, _SZ, _P]),
+    "pkv_decode_timed": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _P, _P,
+                                        _I32, _F32, _I32, _P, _P, _SZ, _P, _P, _P]),
+    "pkv_plan_decode_timed": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
+                                             ctypes.POINTER(PlanParams), _P, _I32, _P, _P, _F32, _P, _P, _SZ,
+                                             _P, _P, _P]),
     "pkv_decode_rect": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _I32, _I32,
                                        _I32, _F32, _P, _P, _SZ, _P]),
     "pkv_decode_buckets": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _P, _I32, _I32, _I32, _I32, _I32,
@@ -143,34 +148,59 @@ def pkv_plan(seq_lens: torch.Tensor, block_table, num_pages: int, params: PlanPa
                                       ws.numel(), _stream(stream)))
 
 
+def _events(events) -> tuple:
+    """(start, stop) torch timing events -> raw handles. torch creates an event's handle
+    on its first record, so each is recorded once here before its handle is taken."""
+    if events is None:
+        return None
+    out = []
+    for ev in events:
+        ev.record()
+        out.append(ev.cuda_event)
+    return tuple(out)
+
+
 def pkv_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
                seq_lens: torch.Tensor, tasks: torch.Tensor, split_offsets: torch.Tensor, num_tasks: torch.Tensor,
-               sm_scale: float, out: torch.Tensor, ws: torch.Tensor, *, fused: bool = True, stream=None):
+               sm_scale: float, out: torch.Tensor, ws: torch.Tensor, *, fused: bool = True, stream=None,
+               events=None):
+    """events: optional (start, stop) timing events stamped with the kernels' execution
+    interval (pkv_decode_timed)."""
     B, Hq, d = q.shape
     num_pages, _, Hkv, _ = k_cache.shape
-    _check("pkv_decode", lib().pkv_decode(
-        _dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
-        _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
-        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d,
-        _dev(tasks, torch.int32, "tasks"), _dev(split_offsets, torch.int32, "split_offsets"),
-        _dev(num_tasks, torch.int32, "num_tasks"), tasks.numel() // TASK_FIELDS, float(sm_scale),
-        PKV_FUSED_MERGE if fused else 0, _dev(out, torch.float16, "out"), _dev(ws, torch.uint8, "ws"),
-        ws.numel(), _stream(stream)))
+    ev = _events(events)
+    args = (_dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
+            _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
+            block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d,
+            _dev(tasks, torch.int32, "tasks"), _dev(split_offsets, torch.int32, "split_offsets"),
+            _dev(num_tasks, torch.int32, "num_tasks"), tasks.numel() // TASK_FIELDS, float(sm_scale),
+            PKV_FUSED_MERGE if fused else 0, _dev(out, torch.float16, "out"), _dev(ws, torch.uint8, "ws"),
+            ws.numel(), _stream(stream))
+    if ev is None:
+        _check("pkv_decode", lib().pkv_decode(*args))
+    else:
+        _check("pkv_decode_timed", lib().pkv_decode_timed(*args, *ev))
 
 
 def pkv_plan_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
                     seq_lens: torch.Tensor, params: PlanParams, tasks: torch.Tensor, split_offsets: torch.Tensor,
-                    num_tasks: torch.Tensor, sm_scale: float, out: torch.Tensor, ws: torch.Tensor, *, stream=None):
+                    num_tasks: torch.Tensor, sm_scale: float, out: torch.Tensor, ws: torch.Tensor, *, stream=None,
+                    events=None):
+    """events: optional (start, stop) timing events (pkv_plan_decode_timed)."""
     B, Hq, d = q.shape
     num_pages, _, Hkv, _ = k_cache.shape
-    _check("pkv_plan_decode", lib().pkv_plan_decode(
-        _dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
-        _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
-        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d, ctypes.byref(params),
-        _dev(tasks, torch.int32, "tasks"), tasks.numel() // TASK_FIELDS, _dev(split_offsets, torch.int32,
-                                                                                "split_offsets"),
-        _dev(num_tasks, torch.int32, "num_tasks"), float(sm_scale), _dev(out, torch.float16, "out"),
-        _dev(ws, torch.uint8, "ws"), ws.numel(), _stream(stream)))
+    ev = _events(events)
+    args = (_dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
+            _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
+            block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d, ctypes.byref(params),
+            _dev(tasks, torch.int32, "tasks"), tasks.numel() // TASK_FIELDS,
+            _dev(split_offsets, torch.int32, "split_offsets"), _dev(num_tasks, torch.int32, "num_tasks"),
+            float(sm_scale), _dev(out, torch.float16, "out"), _dev(ws, torch.uint8, "ws"), ws.numel(),
+            _stream(stream))
+    if ev is None:
+        _check("pkv_plan_decode", lib().pkv_plan_decode(*args))
+    else:
+        _check("pkv_plan_decode_timed", lib().pkv_plan_decode_timed(*args, *ev))
 
 
 def _host_i32(x) -> tuple:

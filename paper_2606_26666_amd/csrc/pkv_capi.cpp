@@ -140,11 +140,11 @@ int pkv_plan(const int32_t* seq_lens, const int32_t* block_table, int32_t B, int
   return from_hip(launch_plan(a, stream));
 }
 
-int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
-               const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
-               int32_t Hq, int32_t Hkv, int32_t d, const pkv_task* tasks, const int32_t* split_offsets,
-               const int32_t* num_tasks, int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out,
-               void* ws, size_t ws_bytes, hipStream_t stream) {
+int pkv_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                     const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
+                     int32_t Hq, int32_t Hkv, int32_t d, const pkv_task* tasks, const int32_t* split_offsets,
+                     const int32_t* num_tasks, int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out,
+                     void* ws, size_t ws_bytes, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
   int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
   if (st != PKV_OK) return st;
   if (!tasks || !split_offsets || !num_tasks || !aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
@@ -163,7 +163,17 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
   a.max_tasks = max_tasks;
   // grid: max_tasks, capped at the workgroups the device holds at once (each workgroup
   // loops over tasks with the grid as stride)
-  return from_hip(launch_decode(a, G, flags == PKV_FUSED_MERGE ? 1 : 0, max_tasks, stream));
+  return from_hip(launch_decode(a, G, flags == PKV_FUSED_MERGE ? 1 : 0, max_tasks, stream, start, stop));
+}
+
+int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+               const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
+               int32_t Hq, int32_t Hkv, int32_t d, const pkv_task* tasks, const int32_t* split_offsets,
+               const int32_t* num_tasks, int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out,
+               void* ws, size_t ws_bytes, hipStream_t stream) {
+  return pkv_decode_timed(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq, Hkv,
+                          d, tasks, split_offsets, num_tasks, max_tasks, sm_scale, flags, out, ws, ws_bytes, stream,
+                          nullptr, nullptr);
 }
 
 int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
@@ -287,11 +297,12 @@ int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s
   return from_hip(launch_read(src, bytes, sink, stream));
 }
 
-int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
-                    const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
-                    int32_t Hq, int32_t Hkv, int32_t d, const pkv_plan_params* params, pkv_task* tasks,
-                    int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
-                    void* ws, size_t ws_bytes, hipStream_t stream) {
+int pkv_plan_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                          const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens,
+                          int32_t B, int32_t Hq, int32_t Hkv, int32_t d, const pkv_plan_params* params,
+                          pkv_task* tasks, int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks,
+                          float sm_scale, uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop) {
   int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
   if (st != PKV_OK) return st;
   int G = 0;
@@ -312,7 +323,17 @@ int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
   a.num_tasks = num_tasks;
   a.max_tasks = max_tasks;
   a.plan = pa;
-  return from_hip(launch_decode(a, G, 3, max_tasks, stream));
+  return from_hip(launch_decode(a, G, 3, max_tasks, stream, start, stop));
+}
+
+int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                    const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B,
+                    int32_t Hq, int32_t Hkv, int32_t d, const pkv_plan_params* params, pkv_task* tasks,
+                    int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
+                    void* ws, size_t ws_bytes, hipStream_t stream) {
+  return pkv_plan_decode_timed(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
+                               Hkv, d, params, tasks, max_tasks, split_offsets, num_tasks, sm_scale, out, ws,
+                               ws_bytes, stream, nullptr, nullptr);
 }
 
 }  // extern "C"

@@ -65,7 +65,9 @@ struct DecodeArgs {
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 // mode: 0 split + merge kernels, 1 fused merge, 2 rectangular split + merge,
 //       3 plan + split + fused merge in one launch
-hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s);
+// start/stop (may be null): stamped when the call's first kernel starts and its last ends
+hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s,
+                         hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s);

@@ -16,6 +16,7 @@
 // Each of the four lane rows then runs its own online softmax (m, l, acc[G][8 dims]) in
 // fp32 over the tokens it saw. At the end of the task a lane butterfly combines the
 // four rows of each wavefront and LDS combines the W wavefront states, in a fixed order.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "pkv_internal.h"
@@ -1105,47 +1106,51 @@ int resident_blocks(const void* kernel, int threads) {
   return per_cu * cus;
 }
 
+// Kernels go out through hipExtLaunchKernelGGL: with events it stamps `start` when the
+// first kernel of the call begins and `stop` when the last one ends (kernel execution
+// time, as a profiler reports it); without events it is a plain launch.
+template <typename K>
+hipError_t launch(K kernel, int grid, int threads, hipStream_t s, hipEvent_t start, hipEvent_t stop,
+                  const DecodeArgs& a) {
+  hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, s, start, stop, 0, a);
+  return hipGetLastError();
+}
+
 template <int G, int W>
-hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t s) {
+hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t s, hipEvent_t start,
+                           hipEvent_t stop) {
   if (mode == 2) {
     const int rows = a.n_rows > 0 ? a.n_rows : a.B;
-    hipLaunchKernelGGL((rect_kernel<G, W>), dim3(rows * a.Hkv * a.S), dim3(W * 64), 0, s, a);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch(rect_kernel<G, W>, rows * a.Hkv * a.S, W * 64, s, start, nullptr, a);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((merge_kernel<G, true>), dim3(rows * a.Hkv), dim3(kMergeThreads), 0, s, a);
-    return hipGetLastError();
+    return launch(merge_kernel<G, true>, rows * a.Hkv, kMergeThreads, s, nullptr, stop, a);
   }
   if (mode == 1) {
     static const int resident = resident_blocks((const void*)split_kernel<G, W, true, false>, W * 64);
-    grid = grid < resident ? grid : resident;
-    hipLaunchKernelGGL((split_kernel<G, W, true, false>), dim3(grid), dim3(W * 64), 0, s, a);
-    return hipGetLastError();
+    return launch(split_kernel<G, W, true, false>, grid < resident ? grid : resident, W * 64, s, start, stop, a);
   }
   if (mode == 3) {
     static const int resident = resident_blocks((const void*)split_kernel<G, W, true, true>, W * 64);
-    grid = grid < resident ? grid : resident;
-    hipLaunchKernelGGL((split_kernel<G, W, true, true>), dim3(grid), dim3(W * 64), 0, s, a);
-    return hipGetLastError();
+    return launch(split_kernel<G, W, true, true>, grid < resident ? grid : resident, W * 64, s, start, stop, a);
   }
   static const int resident = resident_blocks((const void*)split_kernel<G, W, false, false>, W * 64);
-  grid = grid < resident ? grid : resident;
-  hipLaunchKernelGGL((split_kernel<G, W, false, false>), dim3(grid), dim3(W * 64), 0, s, a);
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch(split_kernel<G, W, false, false>, grid < resident ? grid : resident, W * 64, s, start,
+                        nullptr, a);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((merge_kernel<G, false>), dim3(a.B * a.Hkv), dim3(kMergeThreads), 0, s, a);
-  return hipGetLastError();
+  return launch(merge_kernel<G, false>, a.B * a.Hkv, kMergeThreads, s, nullptr, stop, a);
 }
 
 }  // namespace
 
 constexpr int kWaves = 4;
 
-hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s) {
+hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s, hipEvent_t start,
+                         hipEvent_t stop) {
   switch (G) {
-    case 1: return launch_decode_g<1, kWaves>(a, mode, grid, s);
-    case 2: return launch_decode_g<2, kWaves>(a, mode, grid, s);
-    case 4: return launch_decode_g<4, kWaves>(a, mode, grid, s);
-    case 8: return launch_decode_g<8, kWaves>(a, mode, grid, s);
+    case 1: return launch_decode_g<1, kWaves>(a, mode, grid, s, start, stop);
+    case 2: return launch_decode_g<2, kWaves>(a, mode, grid, s, start, stop);
+    case 4: return launch_decode_g<4, kWaves>(a, mode, grid, s, start, stop);
+    case 8: return launch_decode_g<8, kWaves>(a, mode, grid, s, start, stop);
     default: return hipErrorInvalidValue;
   }
 }
