@@ -101,12 +101,17 @@ class Runner:
         self.gen.manual_seed(seed * 4 + 3)
         self.bt_host = w.block_table
 
+    def shape(self, lens):
+        """The cost model's account of one step of this route over `lens`."""
+        from paper_2606_26666_amd import costmodel
+        return costmodel.route_shape(self.route, lens, self.params, self.w.hq, self.w.head_dim,
+                                     self.w.max_pages_per_row)
+
     def rect_splits(self):
-        """Split count of the rectangular grid: the batch rule of the planner's policy 0,
-        S = clamp(ceil(target / (B_active * Hkv)), split_min, split_max), on the host."""
-        p, w = self.params, self.w
-        active = max(1, int(np.count_nonzero(np.asarray(self.cur_lens) > 0)))
-        return int(min(max(-(-p.target_tasks // (active * w.hkv)), p.split_min), p.split_max))
+        """Split count of the rectangular grid (the cost model's batch rule)."""
+        from paper_2606_26666_amd import costmodel
+        active = int(np.count_nonzero(np.asarray(self.cur_lens) > 0))
+        return costmodel.rect_split_count(active, self.w.hkv, self.params)
 
     def host_lengths(self, step):
         return self.w.lengths_at(step)
@@ -191,7 +196,7 @@ def measure(runner, steps, warmup, flush_bufs):
         e2.record()
         ev.append((e0, e2))
         ntasks.append(runner.bufs.num_tasks.clone() if runner.route in ("one-launch", "plan+fused", "two-kernel")
-                      else route_slots(runner, runner.cur_lens)[0])
+                      else runner.shape(runner.cur_lens).workgroups)
     torch.cuda.synchronize()
     step_ms = [a.elapsed_time(c) for a, c in ev]
     ntasks = [int(t.item()) if hasattr(t, "item") else int(t) for t in ntasks]
@@ -308,41 +313,18 @@ def summarize(runner, m):
 def launches_per_step(runner):
     if runner.route in ("exact-buckets", "coarse-buckets"):
         return runner.last_launches
-    return {"one-launch": 1, "plan+fused": 2, "two-kernel": 3, "rect": 2}[runner.route]
-
-
-def route_slots(runner, lens):
-    """(split workgroups = partial-state slots, merge launches) of the host-planned routes
-    for one step's lengths: the rectangular grid and the length buckets."""
-    w, p = runner.w, runner.params
-    lens = np.asarray(lens, dtype=np.int64)
-    if runner.route == "rect":
-        return len(lens) * w.hkv * runner.rect_splits(), 1
-    keys = [(-1 if n == 0 else (n if runner.route == "exact-buckets" else -(-n // BUCKET_TOKENS))) for n in lens]
-    wgs = groups = 0
-    for k in sorted(set(keys)):
-        nb = keys.count(k)
-        for c in range(0, nb, 64):
-            n = min(64, nb - c)
-            S = min(max(-(-p.target_tasks // (n * w.hkv)), p.split_min), p.split_max)
-            wgs += n * w.hkv * S
-            groups += 1
-    return wgs, groups
+    return runner.shape(runner.cur_lens).launch_count
 
 
 def route_counters(runner, m):
-    """Scheduler-derived counters of the paper's Tab. 4 for the last timed step: split
-    workgroups per CU (256 CUs), useful KV MiB, partial-state (merge) MiB, merge launches."""
-    w = runner.w
+    """Scheduler counters of the paper's Tab. 4 for the last timed step (from the cost
+    model's route shape): split workgroups per CU, useful KV MiB, partial-state (merge)
+    MiB, merge launches."""
     lens = np.asarray(m["lens"][-1], dtype=np.int64)
-    if runner.route in ("rect", "exact-buckets", "coarse-buckets"):
-        wgs, merge_launches = route_slots(runner, lens)
-        slots = wgs
-    else:
-        wgs = slots = m["ntasks"][-1]
-        merge_launches = 1 if runner.route == "two-kernel" else 0
-    return {"split_wg_per_cu": wgs / 256.0, "useful_kv_mib": float(lens.sum()) * KV_BYTES_PER_TOKEN / 2**20,
-            "merge_mib": slots * SLOT_BYTES / 2**20, "merge_launches": merge_launches}
+    sh = runner.shape(lens)
+    return {"split_wg_per_cu": sh.workgroups / 256.0,
+            "useful_kv_mib": float(lens.sum()) * KV_BYTES_PER_TOKEN / 2**20,
+            "merge_mib": sh.merge_bytes / 2 / 2**20, "merge_launches": sh.merge_launches}
 
 
 def read_traffic(workload):
@@ -406,6 +388,59 @@ def cpu_baseline(runner, steps, budget_s=15.0):
             "tiny_step_ms": dt_tiny * 1e3}
 
 
+CALIBRATION = os.path.join(ROOT, "paper_2606_26666_amd", "calibration_mi355x.json")
+# (workload, route, policy, task target) steps the cost model is fitted on: the split
+# sensitivity sweep of the one-launch workqueue plus every other route on the ragged
+# B8 trace and on B1 (exact buckets are left out: their step time includes host launch
+# time whenever the host falls behind)
+CAL_RUNS = ([(w, "one-launch", 1, t) for w in ("b1", "b8_bimodal") for t in (128, 256, 512, 1024)]
+            + [(w, "one-launch", 1, 256) for w in ("b8_uniform", "b8_zipf", "b4_bimodal")]
+            + [("b8_bimodal", r, 1, 256) for r in ("plan+fused", "two-kernel")]
+            + [(w, r, 0, 256) for w in ("b8_bimodal", "b8_uniform", "b1") for r in ("rect", "coarse-buckets")])
+
+
+def dataclass_dict(x):
+    import dataclasses
+    return dataclasses.asdict(x)
+
+
+def fit_cost_model(args, flush_bufs, probe, out_path):
+    """Time every CAL_RUNS configuration, fit C_min and T_0 with beta and lambda from the
+    probes, write the calibration file and return (calibration, rows)."""
+    from paper_2606_26666_amd import costmodel
+    samples, rows = [], []
+    for (wl, route, policy, target) in CAL_RUNS:
+        r = Runner(wl, args.seed, target, 50 if wl != "b1" else 20, route=route, policy=policy)
+        m = measure(r, args.steps, args.warmup, flush_bufs)
+        sh = r.shape(m["lens"][-1])
+        us = float(np.mean(m["step_ms"])) * 1e3
+        samples.append((sh, us))
+        rows.append((wl, route, policy, target, sh, us))
+        del r
+    cal = costmodel.fit(samples, probe["beta_read_gbs"], probe["launch_gap_us"])
+    cal.note += f"; written by: python bench.py --calibrate {os.path.relpath(out_path, ROOT)}"
+    cal.save(out_path)
+    table = [{"workload": wl, "route": route, "policy": pol, "target": t, "measured_us": us,
+              "model_us": costmodel.estimate_us(sh, cal), "wg_per_cu": sh.workgroups / 256.0}
+             for (wl, route, pol, t, sh, us) in rows]
+    return cal, table
+
+
+def cost_model_view(runner, measured_us):
+    """The committed calibration's estimate of every route for the runner's last step."""
+    from paper_2606_26666_amd import costmodel
+    if not os.path.exists(CALIBRATION):
+        return None
+    cal = costmodel.Calibration.load(CALIBRATION)
+    lens = runner.cur_lens
+    est = {r: costmodel.estimate_us(costmodel.route_shape(r, lens, runner.params, runner.w.hq, runner.w.head_dim,
+                                                         runner.w.max_pages_per_row), cal)
+           for r in costmodel.ROUTES}
+    return {"chosen": min(est, key=est.get), "estimate_us": est, "measured_us": measured_us,
+            "calibration": {"beta_gbs": cal.beta_gbs, "probe_beta_gbs": cal.probe_beta_gbs,
+                            "launch_us": cal.launch_us, "c_min": cal.c_min, "fixed_us": cal.fixed_us}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -429,6 +464,9 @@ def main():
                          "('none' to skip)")
     ap.add_argument("--no-flush", action="store_true", help="keep KV warm in the last-level cache")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate", metavar="PATH",
+                    help="fit the route cost model (C_min, T_0) on the CAL_RUNS steps, write it to PATH, print "
+                         "measured against modelled step times as one JSON line, and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one MI355X: this build has no multi-GPU path (run with --gpus 1)",
@@ -453,12 +491,17 @@ def main():
                       torch.zeros(1, dtype=torch.int32, device="cuda"))
 
     cal = calibrate(pkv, torch, flush_bufs)
+    if args.calibrate:
+        model, table = fit_cost_model(args, flush_bufs, cal, os.path.abspath(args.calibrate))
+        print(json.dumps({"calibration": dataclass_dict(model), "steps": table}))
+        return
     steps_cfg = max(args.steps, 20 if args.workload == "b1" else 50)
     main_run = Runner(args.workload, args.seed, args.target_tasks, steps_cfg, route=args.route,
                       policy=args.policy)
     m = measure(main_run, args.steps, args.warmup, flush_bufs)
     s = summarize(main_run, m)
-    extra = {args.workload: s, "calibration": cal}
+    extra = {args.workload: s, "calibration": cal,
+             "cost_model": cost_model_view(main_run, s["ms_per_step"] * 1e3)}
     for name in [x for x in args.also.split(",") if x and x != "none" and x != args.workload]:
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))

@@ -133,6 +133,20 @@ int pkv_plan(const int32_t* seq_lens, const int32_t* block_table, int32_t B,
              pkv_task* tasks, int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks,
              void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* The same plan computed on the host (Sec. 3.4-3.5), for buffer sizing and route
+ * costing without a device round trip. Identical task list, split_offsets and count to
+ * pkv_plan on the same lengths and parameters.
+ *   seq_lens      host int32 [B]; every length must lie in [0, max_pages_per_row * 16]
+ *                 (else PKV_ERR_INVALID_ARG: the host reports it at once)
+ *   tasks         host pkv_task [max_tasks], or NULL to compute only the counts
+ *   split_offsets host int32 [B+1], or NULL
+ *   num_tasks     host int32 [1] (always written on success)
+ * PKV_ERR_WORKSPACE when tasks is given and max_tasks < the task count (num_tasks and
+ * split_offsets are still written). */
+int pkv_plan_host(const int32_t* seq_lens, int32_t B, int32_t max_pages_per_row,
+                  const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+                  int32_t* split_offsets, int32_t* num_tasks);
+
 /* Decode attention over the task list (Sec. 3.3-3.4).
  *   q          device fp16 [B, Hq, d]
  *   k_cache, v_cache  device fp16 [num_pages, page_size=16, Hkv, d] (token-major pages)

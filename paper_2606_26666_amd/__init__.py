@@ -28,6 +28,7 @@ from ._binding import (  # noqa: F401
     pkv_decode_rect,
     pkv_max_tasks,
     pkv_plan,
+    pkv_plan_host,
     pkv_plan_decode,
     pkv_stream_copy,
     pkv_stream_read,

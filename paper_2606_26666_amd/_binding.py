@@ -51,6 +51,7 @@ _SIGS = {
     "pkv_workspace_init": (ctypes.c_int, [_P, _SZ, _I32, _I32, _P]),
     "pkv_plan": (ctypes.c_int, [_P, _P, _I32, _I32, _I32, ctypes.POINTER(PlanParams), _P, _I32, _P, _P,
                                 _P, _SZ, _P]),
+    "pkv_plan_host": (ctypes.c_int, [_P, _I32, _I32, ctypes.POINTER(PlanParams), _P, _I32, _P, _P]),
     "pkv_decode": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _P, _P, _I32,
                                   _F32, _I32, _P, _P, _SZ, _P]),
     "pkv_plan_decode": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
@@ -146,6 +147,25 @@ def pkv_plan(seq_lens: torch.Tensor, block_table, num_pages: int, params: PlanPa
                                       _dev(split_offsets, torch.int32, "split_offsets"),
                                       _dev(num_tasks, torch.int32, "num_tasks"), _dev(ws, torch.uint8, "ws"),
                                       ws.numel(), _stream(stream)))
+
+
+def pkv_plan_host(seq_lens, params: PlanParams, max_pages_per_row: int, with_tasks: bool = True):
+    """Host planner: (tasks int32 [n, 5] or None, split_offsets int32 [B+1], n) from host
+    lengths, identical to the device plan."""
+    import numpy as np
+    lens = np.ascontiguousarray(np.asarray(seq_lens, dtype=np.int32).reshape(-1))
+    B = lens.size
+    offs = np.zeros(B + 1, dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check("pkv_plan_host", lib().pkv_plan_host(lens.ctypes.data, B, int(max_pages_per_row), ctypes.byref(params),
+                                                None, 0, offs.ctypes.data, ctypes.byref(n)))
+    if not with_tasks:
+        return None, offs, n.value
+    tasks = np.zeros((max(1, n.value), TASK_FIELDS), dtype=np.int32)
+    _check("pkv_plan_host", lib().pkv_plan_host(lens.ctypes.data, B, int(max_pages_per_row), ctypes.byref(params),
+                                                tasks.ctypes.data, tasks.shape[0], offs.ctypes.data,
+                                                ctypes.byref(n)))
+    return tasks[:n.value], offs, n.value
 
 
 def _events(events) -> tuple:

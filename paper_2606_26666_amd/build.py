@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libpkv.so")
-SOURCES = ["pkv_kernels.hip", "pkv_capi.cpp"]
+SOURCES = ["pkv_kernels.hip", "pkv_capi.cpp", "pkv_host.cpp"]
 
 # Packed-fp32 instructions stay off: plain fp32 ops only (the host pass warns that it
 # does not know the feature; that is harmless).

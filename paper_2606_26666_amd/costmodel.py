@@ -1,0 +1,170 @@
+"""Route cost model (Sec. 3.5), fitted to this GPU.
+
+For one decode step over lengths N_i, route r is priced as
+
+    T_r = sum_j KV_j / beta * max(1, C_min / C_j) + L_r * lambda + Merge_r / beta + T_0
+
+where the sum runs over the route's split launches j (one for the workqueue routes and
+the rectangular grid, one per group for the length buckets), KV_j is the K/V bytes launch
+j streams, C_j its split workgroups per compute unit, L_r the launches per step, Merge_r
+the partial-state bytes written and read back, beta the streaming-read bandwidth and
+lambda the device time per launch. The first three terms are the paper's model. T_0 is
+added here: on MI355X every step also pays a fixed chain of memory round trips (lengths,
+page ids, first pages, state store, completion counter, merge) of roughly 10 us that no
+term of the paper's model captures. lambda is measured by a probe; C_min, T_0 and the
+effective beta (the KV stream of a step runs below the probe's streaming-read rate, which
+is kept beside it) are fitted to measured steps (`fit`).
+
+Everything here is host arithmetic over the planner's counts (`pkv_plan_host`); it
+launches nothing.
+"""
+from __future__ import annotations
+
+import dataclasses
+import json
+import math
+
+import numpy as np
+
+from . import _binding as _b
+
+ROUTES = ("one-launch", "plan+fused", "two-kernel", "rect", "exact-buckets", "coarse-buckets")
+LAUNCHES = {"one-launch": 1, "plan+fused": 2, "two-kernel": 3}
+MAX_BUCKET_ROWS = 64   # rows one rectangular launch can name
+COARSE_BUCKET_TOKENS = 16384
+
+
+@dataclasses.dataclass
+class Calibration:
+    beta_gbs: float          # effective KV streaming bandwidth of a step, GB/s
+    launch_us: float         # device time per back-to-back launch, us
+    c_min: float = 1.0       # occupancy (split workgroups per CU) below which KV streams slower
+    fixed_us: float = 0.0    # per-step fixed latency T_0, us
+    cus: int = 256           # compute units
+    probe_beta_gbs: float = 0.0  # streaming-read bandwidth of the probe (a 1 GiB read), GB/s
+    note: str = ""
+
+    def save(self, path: str) -> None:
+        with open(path, "w") as f:
+            json.dump(dataclasses.asdict(self), f, indent=2, sort_keys=True)
+            f.write("\n")
+
+    @classmethod
+    def load(cls, path: str) -> "Calibration":
+        with open(path) as f:
+            d = json.load(f)
+        names = [fld.name for fld in dataclasses.fields(cls)]
+        return cls(**{k: d[k] for k in names if k in d})
+
+
+@dataclasses.dataclass
+class RouteShape:
+    """What a route does in one step: per split launch (KV bytes, split workgroups), the
+    launch count and the partial-state bytes written and read."""
+    launches: list            # [(kv_bytes, workgroups)] per split launch
+    launch_count: int
+    merge_bytes: int
+    merge_launches: int
+
+    @property
+    def workgroups(self) -> int:
+        return int(sum(w for _, w in self.launches))
+
+
+def slot_bytes(G: int, d: int = 128) -> int:
+    """Partial-state slot: fp32 acc[G][d], m[G], l[G], padded to 16 bytes."""
+    return 4 * (G * d + ((2 * G + 3) // 4) * 4)
+
+
+def rect_split_count(n_rows: int, hkv: int, params) -> int:
+    """One split count for a rectangular launch over n_rows rows (the batch rule)."""
+    s = -(-params.target_tasks // (max(1, n_rows) * hkv))
+    return int(min(max(s, params.split_min), params.split_max))
+
+
+def bucket_groups(lens, exact: bool, bucket_tokens: int = COARSE_BUCKET_TOKENS):
+    """Row groups of the bucket routes, as pkv_decode_buckets forms them: rows keyed by
+    exact length or by ceil(length / bucket_tokens) (empty rows form their own group,
+    launched so that their output is written as zeros), each key split into launches of
+    at most 64 rows. Returns a list of row-index arrays."""
+    lens = np.asarray(lens, dtype=np.int64)
+    keys = np.where(lens == 0, -1, lens if exact else -(-lens // bucket_tokens))
+    groups = []
+    for k in sorted(set(keys.tolist())):
+        rows = np.nonzero(keys == k)[0]
+        for c in range(0, rows.size, MAX_BUCKET_ROWS):
+            groups.append(rows[c:c + MAX_BUCKET_ROWS])
+    return groups
+
+
+def route_shape(route: str, lens, params, hq: int = 32, d: int = 128,
+                max_pages_per_row: int | None = None) -> RouteShape:
+    """Counts of one step of `route` over lengths `lens` with planner parameters `params`."""
+    lens = np.asarray(lens, dtype=np.int64)
+    hkv = params.num_kv_heads
+    G = hq // hkv
+    kv_tok = 2 * hkv * d * 2
+    sb = slot_bytes(G, d)
+    kv = int(lens.sum()) * kv_tok
+    if route in LAUNCHES:
+        maxp = max_pages_per_row or int(lens.max(initial=0)) // 16 + 1
+        _, _, n = _b.pkv_plan_host(lens, params, maxp, with_tasks=False)
+        return RouteShape([(kv, n)], LAUNCHES[route], 2 * n * sb, 1 if route == "two-kernel" else 0)
+    if route == "rect":
+        active = int(np.count_nonzero(lens))
+        slots = lens.size * hkv * rect_split_count(active, hkv, params)
+        return RouteShape([(kv, slots)], 2, 2 * slots * sb, 1)
+    if route in ("exact-buckets", "coarse-buckets"):
+        launches, slots = [], 0
+        groups = bucket_groups(lens, route == "exact-buckets")
+        for rows in groups:
+            s = rows.size * hkv * rect_split_count(rows.size, hkv, params)
+            launches.append((int(lens[rows].sum()) * kv_tok, s))
+            slots += s
+        return RouteShape(launches, 2 * len(groups), 2 * slots * sb, len(groups))
+    raise ValueError(f"unknown route {route}")
+
+
+def estimate_us(shape: RouteShape, cal: Calibration) -> float:
+    """T_r of the module docstring, in microseconds."""
+    bw = cal.beta_gbs * 1e3  # bytes per microsecond
+    t = 0.0
+    for kv, wgs in shape.launches:
+        c = wgs / cal.cus
+        t += kv / bw * max(1.0, cal.c_min / c) if c > 0 else 0.0
+    return t + shape.launch_count * cal.launch_us + shape.merge_bytes / bw + cal.fixed_us
+
+
+def choose_route(lens, params, cal: Calibration, routes=ROUTES, **kw):
+    """(cheapest route, {route: estimated us}) for one step."""
+    est = {r: estimate_us(route_shape(r, lens, params, **kw), cal) for r in routes}
+    return min(est, key=est.get), est
+
+
+def fit(samples, probe_beta_gbs: float, launch_us: float, cus: int = 256,
+        c_grid=None, beta_scales=None) -> Calibration:
+    """Fit C_min, T_0 and the effective beta to measured steps, lambda fixed by its probe.
+
+    samples: [(RouteShape, measured_us)]. On a grid of (beta, C_min) the best T_0 is the
+    mean residual (least squares in T_0); the pair with the smallest squared error wins.
+    beta is searched as a fraction of the probe's streaming-read bandwidth.
+    """
+    if not samples:
+        raise ValueError("no samples")
+    if c_grid is None:
+        c_grid = np.round(np.arange(0.05, 8.0001, 0.05), 4)
+    if beta_scales is None:
+        beta_scales = np.round(np.arange(0.60, 1.1001, 0.01), 4)
+    best = None
+    for bs in beta_scales:
+        for c in c_grid:
+            base = Calibration(probe_beta_gbs * float(bs), launch_us, float(c), 0.0, cus)
+            resid = np.array([m - estimate_us(sh, base) for sh, m in samples])
+            t0 = float(resid.mean())
+            err = float(((resid - t0) ** 2).sum())
+            if best is None or err < best[0] - 1e-9:
+                best = (err, float(bs), float(c), t0)
+    err, bs, c, t0 = best
+    rms = math.sqrt(err / len(samples))
+    return Calibration(probe_beta_gbs * bs, launch_us, c, t0, cus, probe_beta_gbs,
+                       note=f"fit over {len(samples)} steps, rms {rms:.2f} us")

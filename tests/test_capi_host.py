@@ -156,3 +156,48 @@ def test_plan_decode_validation():
     assert pd(params=b.PlanParams(16, 32, 4, 16, 64, 512)) == pkv.PKV_ERR_INVALID_ARG   # Hkv mismatch
     assert pd(max_tasks=100) == pkv.PKV_ERR_WORKSPACE
     assert pd(ws_bytes=4096) == pkv.PKV_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_host_planner_matches_oracle(policy):
+    """pkv_plan_host (C++) against the oracle's ref_plan: bit-exact task lists and offsets."""
+    import numpy as np
+
+    from oracle import PlanParams, ref_plan
+    lib()
+    r = np.random.Generator(np.random.PCG64(7 + policy))
+    for trial in range(60):
+        B = int(r.integers(1, 300)) if trial % 3 else int(r.integers(1, 9))
+        lens = r.integers(0, 70000, size=B).astype(np.int32)
+        lens[r.random(B) < 0.2] = 0
+        hkv = int(r.choice([1, 2, 4, 8]))
+        smin = int(r.integers(1, 17))
+        smax = smin + int(r.integers(0, 100))
+        target = int(r.integers(1, 5000))
+        tile = int(r.choice([16, 32, 64]))
+        maxp = int(lens.max()) // 16 + 1
+        p = pkv.make_params(hkv, smin, smax, target, tile, policy=policy)
+        tasks, offs, n = pkv.pkv_plan_host(lens, p, maxp)
+        rt, ro, _ = ref_plan(lens, PlanParams(16, tile, hkv, smin, smax, target, policy), max_pages_per_row=maxp)
+        assert n == len(rt) and np.array_equal(tasks, rt) and np.array_equal(offs, ro), (trial, B, policy)
+
+
+def test_host_planner_validation():
+    import numpy as np
+    L = lib()
+    p = b.PlanParams(16, 32, 8, 16, 64, 512)
+    lens = np.array([100, 40], dtype=np.int32)
+    n = ctypes.c_int32(-1)
+    assert L.pkv_plan_host(lens.ctypes.data, 2, 10, ctypes.byref(p), None, 0, None, ctypes.byref(n)) == pkv.PKV_OK
+    assert n.value == 8 * (4 + 2)                         # S = 32 caps nothing: 4 + 2 splits
+    assert L.pkv_plan_host(lens.ctypes.data, 2, 6, ctypes.byref(p), None, 0, None, ctypes.byref(n)) \
+        == pkv.PKV_ERR_INVALID_ARG                        # 100 tokens > 6 pages
+    bad = np.array([-1], dtype=np.int32)
+    assert L.pkv_plan_host(bad.ctypes.data, 1, 10, ctypes.byref(p), None, 0, None, ctypes.byref(n)) \
+        == pkv.PKV_ERR_INVALID_ARG
+    tasks = np.zeros((3, 5), dtype=np.int32)
+    assert L.pkv_plan_host(lens.ctypes.data, 2, 10, ctypes.byref(p), tasks.ctypes.data, 3, None,
+                           ctypes.byref(n)) == pkv.PKV_ERR_WORKSPACE
+    assert L.pkv_plan_host(lens.ctypes.data, 2, 10, ctypes.byref(b.PlanParams(16, 24, 8, 16, 64, 512)), None, 0,
+                           None, ctypes.byref(n)) == pkv.PKV_ERR_UNSUPPORTED
+    assert L.pkv_plan_host(0, 2, 10, ctypes.byref(p), None, 0, None, ctypes.byref(n)) == pkv.PKV_ERR_INVALID_ARG
