@@ -44,8 +44,6 @@ METRIC = "decode tokens/sec per step + achieved HBM GB/s (% of MI355X peak), B1/
 HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_26666_amd", "csrc", "pkv_kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
-KV_BYTES_PER_TOKEN = 2 * 8 * 128 * 2   # K and V, Hkv=8, d=128, fp16
-SLOT_BYTES = 2080                      # fp32 m[4], l[4], acc[4][128]
 TASK_BYTES = 20
 BUCKET_TOKENS = 16384   # coarse-bucket width: rows grouped by ceil(len / 16384)
 ROUTES = ("plan+fused", "one-launch", "two-kernel", "rect", "exact-buckets", "coarse-buckets")
@@ -55,23 +53,29 @@ def kernel_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def algorithmic_bytes(lens, num_tasks, hq=32, d=128):
+def kv_bytes_per_token(hkv=8, d=128):
+    return 2 * hkv * d * 2   # K and V, fp16
+
+
+def algorithmic_bytes(lens, num_tasks, hq=32, d=128, hkv=8):
     """Bytes one decode-kernel launch must move: K/V of every attended token, Q and out,
     the block-table entries and lengths read, the task list, and each task's partial
-    state written once and read once by the merge."""
+    state (fp32 acc[G][d], m[G], l[G]; 2080 B at G=4) written once and read once by the
+    merge."""
+    from paper_2606_26666_amd.costmodel import slot_bytes
     lens = np.asarray(lens, dtype=np.int64)
     B = lens.size
-    kv = KV_BYTES_PER_TOKEN * int(lens.sum())
+    kv = kv_bytes_per_token(hkv, d) * int(lens.sum())
     qo = 2 * B * hq * d * 2
     meta = 4 * int(((lens + 15) // 16).sum()) + 4 * B + 4 * (B + 1) + TASK_BYTES * num_tasks
-    partial = 2 * SLOT_BYTES * num_tasks
+    partial = 2 * slot_bytes(hq // hkv, d) * num_tasks
     return kv + qo + meta + partial, kv
 
 
 class Runner:
     """Device state of one workload: pools, block table, lengths, buffers."""
 
-    def __init__(self, name, seed, target_tasks, steps, route="plan+fused", policy=0):
+    def __init__(self, name, seed, target_tasks, steps, route="plan+fused", policy=0, hkv=8):
         import torch
 
         import paper_2606_26666_amd as pkv
@@ -79,7 +83,7 @@ class Runner:
         from workloads.values import device_normal_f16, q_values
 
         self.torch, self.pkv = torch, pkv
-        self.w = w = make_workload(name, seed=seed, steps=steps, target_tasks=target_tasks)
+        self.w = w = make_workload(name, seed=seed, steps=steps, target_tasks=target_tasks, hkv=hkv)
         self.dev = torch.device("cuda:0")
         shape = (w.num_pages, w.page_size, w.hkv, w.head_dim)
         self.k = device_normal_f16(shape, seed * 4 + 1, self.dev)
@@ -285,7 +289,7 @@ def summarize(runner, m):
     w = runner.w
     tokens = w.batch * len(m["step_ms"])
     step_s = sum(m["step_ms"]) / 1e3
-    alg, kv = zip(*(algorithmic_bytes(l, t, w.hq, w.head_dim) for l, t in zip(m["lens"], m["ntasks"])))
+    alg, kv = zip(*(algorithmic_bytes(l, t, w.hq, w.head_dim, w.hkv) for l, t in zip(m["lens"], m["ntasks"])))
     marker = float(np.median(m["marker_ms"]))
     # decode-kernel duration: its execution interval as stamped by the launch (the
     # duration rocprofv3 reports); the empty-interval marker latency is reported beside it
@@ -323,7 +327,7 @@ def route_counters(runner, m):
     lens = np.asarray(m["lens"][-1], dtype=np.int64)
     sh = runner.shape(lens)
     return {"split_wg_per_cu": sh.workgroups / 256.0,
-            "useful_kv_mib": float(lens.sum()) * KV_BYTES_PER_TOKEN / 2**20,
+            "useful_kv_mib": float(lens.sum()) * kv_bytes_per_token(runner.w.hkv, runner.w.head_dim) / 2**20,
             "merge_mib": sh.merge_bytes / 2 / 2**20, "merge_launches": sh.merge_launches}
 
 
@@ -464,6 +468,8 @@ def main():
                          "('none' to skip)")
     ap.add_argument("--no-flush", action="store_true", help="keep KV warm in the last-level cache")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--hkv", type=int, default=8, choices=(4, 8, 16, 32),
+                    help="KV heads (Hq = 32, so G = 32 / hkv: 8 -> G=4, 32 -> G=1, 4 -> G=8)")
     ap.add_argument("--calibrate", metavar="PATH",
                     help="fit the route cost model (C_min, T_0) on the CAL_RUNS steps, write it to PATH, print "
                          "measured against modelled step times as one JSON line, and exit")
@@ -497,25 +503,25 @@ def main():
         return
     steps_cfg = max(args.steps, 20 if args.workload == "b1" else 50)
     main_run = Runner(args.workload, args.seed, args.target_tasks, steps_cfg, route=args.route,
-                      policy=args.policy)
+                      policy=args.policy, hkv=args.hkv)
     m = measure(main_run, args.steps, args.warmup, flush_bufs)
     s = summarize(main_run, m)
     extra = {args.workload: s, "calibration": cal,
              "cost_model": cost_model_view(main_run, s["ms_per_step"] * 1e3)}
     for name in [x for x in args.also.split(",") if x and x != "none" and x != args.workload]:
-        r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy)
+        r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy, hkv=args.hkv)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
         del r
     for wl in [x for x in args.routes_table.split(",") if x and x != "none"]:
         table = {}
         for route in ROUTES:
-            r = Runner(wl, args.seed, args.target_tasks, 50, route=route, policy=args.policy)
+            r = Runner(wl, args.seed, args.target_tasks, 50, route=route, policy=args.policy, hkv=args.hkv)
             res = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
             table[route] = {k: res[k] for k in ("tok_s", "ms_per_step", "launches_per_step", "split_wg_per_cu",
                                                 "useful_kv_mib", "merge_mib", "merge_launches")}
             del r
         extra["routes_" + wl] = table
-    traffic = read_traffic(args.workload)
+    traffic = read_traffic(args.workload) if args.hkv == 8 else None  # the summaries cover Hkv = 8
     line = {
         "metric": METRIC,
         "value": s["tok_s"],

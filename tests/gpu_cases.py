@@ -55,8 +55,8 @@ class Case:
         self.lens_dev = torch.from_numpy(self.lens).to(DEV)
 
     @classmethod
-    def from_workload(cls, name, step=0, seed=20260622, poison=True):
-        w = make_workload(name, seed=seed)
+    def from_workload(cls, name, step=0, seed=20260622, poison=True, hkv=8):
+        w = make_workload(name, seed=seed, hkv=hkv)
         return cls(w.lengths_at(step), hq=w.hq, hkv=w.hkv, seed=seed, poison=poison, device_values=True,
                    block_table=w.block_table, num_pages=w.num_pages), w
 

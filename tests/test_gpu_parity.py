@@ -300,6 +300,19 @@ def test_plan_decode_benchmark_configs(name):
     assert np.array_equal(tasks, oracle_plan(case, p)[0])
 
 
+@pytest.mark.parametrize("name,hkv", [("b1", 32), ("b1", 4), ("b8_bimodal", 32), ("b8_bimodal", 4)])
+def test_plan_decode_gqa_mappings_full_size(name, hkv):
+    """G = 1 (32 KV heads) and G = 8 (4 KV heads) on the benchmark lengths, one launch."""
+    case, w = Case.from_workload(name, hkv=hkv)
+    p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens, policy=1)
+    bufs = bufs_for(case, w.split_max)
+    out = run_plan_decode(case, bufs, p)
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"{name} G={32 // hkv}")
+    tasks, _ = read_plan(bufs)
+    assert np.array_equal(tasks, oracle_plan(case, p)[0])
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
 def test_rect_named_rows_reads_and_writes_by_index():
     case = Case(RAGGED, seed=14)
     bufs = bufs_for(case, 16, rect_splits=16)

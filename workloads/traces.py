@@ -124,8 +124,9 @@ def _build(name, lens, steps, rho, seed, rng_pages, num_pages=None, split=(16, 6
 
 
 def make_workload(name: str, seed: int = 20260622, steps: int | None = None,
-                  target_tasks: int = 256) -> Workload:
-    """The benchmark configurations, as concrete seeded inputs.
+                  target_tasks: int = 256, hkv: int = HKV) -> Workload:
+    """The benchmark configurations, as concrete seeded inputs. `hkv` changes the number
+    of KV heads (Hq stays 32, so G = 32 / hkv); lengths and page tables do not depend on it.
 
     tiny        : B=1, 512 tokens (no append), pool of 64 pages, one split
     b1          : B=1, 32768 tokens, 4096-page pool, 20 steps
@@ -134,6 +135,11 @@ def make_workload(name: str, seed: int = 20260622, steps: int | None = None,
     b8_zipf     : 8 rows min(32768, 256 k), k~Zipf(1.2), rho=0, 50 steps
     b4_bimodal  : 4 rows bimodal, rho=0, 50 steps
     """
+    w = _make(name, seed, steps, target_tasks)
+    return w if hkv == w.hkv else dataclasses.replace(w, hkv=hkv)
+
+
+def _make(name, seed, steps, target_tasks):
     r_len, r_pages = _rngs(seed, 2)
     if name == "tiny":
         return _build(name, [512], 1 if steps is None else steps, 0.0, seed, r_pages,
