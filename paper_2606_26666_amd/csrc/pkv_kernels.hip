@@ -310,6 +310,48 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
 
 // ---------------------------------------------------------------------------------
 // One task: KV head g of `row`, tokens [t0, t1), partial state into `slot`.
+// The task's partial state from the W wave states staged in LDS (m, l, acc per wave
+// and head, page-error flag per wave): a fixed-order combine, stored to slot `slot`.
+template <int G, int W, bool COHERENT>
+__device__ __forceinline__ void finish_task(const DecodeArgs& a, int slot, float* lds) {
+  float* lds_m = lds;                // [W][G]
+  float* lds_l = lds + W * G;        // [W][G]
+  float* lds_acc = lds + 2 * W * G;  // [W][G][D]
+  int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
+
+  bool any_bad = false;
+#pragma unroll
+  for (int w = 0; w < W; ++w) any_bad |= lds_bad[w] != 0;
+  if (any_bad && threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
+
+  constexpr int SB = slot_floats<G>() * 4;
+  const __amdgpu_buffer_rsrc_t pr = slots_rsrc(a, SB);
+  for (int e4 = threadIdx.x; e4 < G * D / 4; e4 += W * 64) {
+    const int h = (e4 * 4) / D;
+    float M = kNegInf;
+#pragma unroll
+    for (int w = 0; w < W; ++w) M = fmaxf(M, lds_m[w * G + h]);
+    const float Mref = (M == kNegInf) ? 0.0f : M;
+    float L = 0.0f;
+    v4f A = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      const float cf = ex2(lds_m[w * G + h] - Mref);
+      const v4f x = *reinterpret_cast<const v4f*>(lds_acc + (size_t)w * G * D + e4 * 4);
+      L = __builtin_fmaf(cf, lds_l[w * G + h], L);
+      A.x = __builtin_fmaf(cf, x.x, A.x);
+      A.y = __builtin_fmaf(cf, x.y, A.y);
+      A.z = __builtin_fmaf(cf, x.z, A.z);
+      A.w = __builtin_fmaf(cf, x.w, A.w);
+    }
+    st_state4<COHERENT>(pr, slot * SB + e4 * 16, A);
+    if ((e4 * 4) % D == 0) {
+      st_state<COHERENT>(pr, slot * SB + (G * D + h) * 4, M);
+      st_state<COHERENT>(pr, slot * SB + (G * D + G + h) * 4, any_bad ? -1.0f : L);
+    }
+  }
+}
+
 template <int G, int W, bool COHERENT>
 __device__ __forceinline__ void run_task(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
                                          float* lds) {
@@ -485,38 +527,198 @@ __device__ __forceinline__ void run_task(const DecodeArgs& a, int row, int g, in
     lds_bad[wave] = bad ? 1 : 0;
   }
   __syncthreads();
+  finish_task<G, W, COHERENT>(a, slot, lds);
+}
 
-  bool any_bad = false;
-#pragma unroll
-  for (int w = 0; w < W; ++w) any_bad |= lds_bad[w] != 0;
-  if (any_bad && threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
+// ---------------------------------------------------------------------------------
+// The same task with both products on the matrix cores (for G = 4 and 8, where the
+// VALU form spends most of its issue slots on Q.K dot products and P.V FMAs).
+//
+// Per 16-token page of the task's KV head, one wave computes
+//   S[16 tokens x 16] = K_page[16 x 128] . Q^T[128 x 16]       (4 x mfma 16x16x32 f16)
+// with the G query heads in columns 0..G-1 (the others zero), and
+//   O^T[128 x 16] += V_page^T[128 x 16 tokens] . P^T[16 tokens x 16]   (16 x mfma 16x16x16 f16:
+//                                                                      P as hi + lo halves)
+// Lane (grp, col) = (lane / 16, lane % 16):
+//   K operand   token col, dims [32 kb + 8 grp, +8): one 16-byte load per kb, native layout
+//   Q operand   head col, dims [32 kb + 8 grp, +8) (zero for col >= G), loaded once
+//   scores      tokens 4 grp + r (r = 0..3) of head col, which is also the P operand
+//   V operand   dims 16 db + col, tokens 4 grp + r: V is staged token-major in LDS and
+//               read back transposed with ds_read_b64_tr_b16 (within 16 lanes, lane i
+//               receives element i % 4 of the rows that lanes 4 j + i / 4 address)
+//   output      dims 16 db + 4 grp + r of head col
+// Every value a lane holds belongs to head col, so the online-softmax max (shared by the
+// four groups of a head, per page) and the rescale are per lane.
+typedef _Float16 h8v __attribute__((ext_vector_type(8)));
+typedef _Float16 h4v __attribute__((ext_vector_type(4)));
+typedef short s4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s4v lds_s4v;
 
-  constexpr int SB = slot_floats<G>() * 4;
-  const __amdgpu_buffer_rsrc_t pr = slots_rsrc(a, SB);
-  for (int e4 = threadIdx.x; e4 < G * D / 4; e4 += W * 64) {
-    const int h = (e4 * 4) / D;
-    float M = kNegInf;
+template <int G>
+constexpr bool mfma_task() {
+  return G == 4 || G == 8;
+}
+
+template <int G, int W, bool COHERENT>
+__device__ __forceinline__ void run_task_mfma(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
+                                              float* lds) {
+  static_assert(G <= 16, "heads fit the 16 MFMA columns");
+  __shared__ v4u vstage[W][P * D / 8];  // one V page of one head per wave: 16 rows of 256 B
+  float* lds_m = lds;                // [W][G]
+  float* lds_l = lds + W * G;        // [W][G]
+  float* lds_acc = lds + 2 * W * G;  // [W][G][D]
+  int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
+
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int grp = lane >> 4;
+  const int col = lane & 15;
+  const int Hkv = a.Hkv;
+  const size_t tok_stride = (size_t)Hkv * D;  // halves between consecutive tokens
+  const size_t page_stride = (size_t)P * tok_stride;
+  const int tok_b = (int)(tok_stride * 2);
+  const int page_bytes = (int)(page_stride * 2);
+
+  v4u qb[4];
+  {
+    const bool hv = col < G;
+    const uint16_t* qh = a.q + ((size_t)row * a.Hq + (size_t)g * G + (hv ? col : 0)) * D;
 #pragma unroll
-    for (int w = 0; w < W; ++w) M = fmaxf(M, lds_m[w * G + h]);
-    const float Mref = (M == kNegInf) ? 0.0f : M;
-    float L = 0.0f;
-    v4f A = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int w = 0; w < W; ++w) {
-      const float cf = ex2(lds_m[w * G + h] - Mref);
-      const v4f x = *reinterpret_cast<const v4f*>(lds_acc + (size_t)w * G * D + e4 * 4);
-      L = __builtin_fmaf(cf, lds_l[w * G + h], L);
-      A.x = __builtin_fmaf(cf, x.x, A.x);
-      A.y = __builtin_fmaf(cf, x.y, A.y);
-      A.z = __builtin_fmaf(cf, x.z, A.z);
-      A.w = __builtin_fmaf(cf, x.w, A.w);
-    }
-    st_state4<COHERENT>(pr, slot * SB + e4 * 16, A);
-    if ((e4 * 4) % D == 0) {
-      st_state<COHERENT>(pr, slot * SB + (G * D + h) * 4, M);
-      st_state<COHERENT>(pr, slot * SB + (G * D + G + h) * 4, any_bad ? -1.0f : L);
+    for (int kb = 0; kb < 4; ++kb) {
+      const v4u z = {0u, 0u, 0u, 0u};
+      qb[kb] = hv ? *reinterpret_cast<const v4u*>(qh + kb * 32 + 8 * grp) : z;
     }
   }
+  float m = kNegInf, l = 0.0f;
+  v4f acc[D / 16];
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) acc[db] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+
+  const int pg_begin = t0 / P;
+  const int pg_end = (t1 + P - 1) / P;
+  const int* bt = a.block_table + (size_t)row * a.max_pages_per_row;
+  const int k_off = col * tok_b + g * D * 2 + grp * 16;  // + 64 kb
+  const int v_off = grp * tok_b + g * D * 2 + col * 16;  // + 4 i tok_b
+  const int v_step = 4 * tok_b;
+  const int first = pg_begin + wave;
+  const int npw = first < pg_end ? (pg_end - first + W - 1) / W : 0;
+  bool bad = false;
+  v4u* vst = &vstage[wave][0];
+  const int tr_off = (4 * grp + (col >> 2)) * (D * 2) + (col & 3) * 8;  // + 32 db
+
+  int ids = 0;
+  auto issue = [&](v4u (&kr)[4], v4u (&vr)[4], int j) {
+    int phys = __builtin_amdgcn_readlane(ids, j);
+    if (phys < 0 || phys >= a.num_pages) {
+      bad = true;
+      phys = 0;
+    }
+    const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, page_bytes);
+    const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, page_bytes);
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) kr[kb] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, k_off, kb * 64, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, v_off, i * v_step, 0);
+  };
+  auto consume = [&](v4u (&kr)[4], v4u (&vr)[4], int k) {
+    const int pg = first + k * W;
+    const bool tail = pg * P + P > t1;  // the row's last, partial page
+    v4f sc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[kb]), __builtin_bit_cast(h8v, qb[kb]),
+                                                  sc, 0, 0, 0);
+    // stage V token-major; rows past t1 are zeroed (their p is 0, but 0 * NaN is not)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v4u v = vr[i];
+      if (tail && pg * P + 4 * i + grp >= t1) v = v4u{0u, 0u, 0u, 0u};
+      vst[(4 * i + grp) * (D / 8) + col] = v;
+    }
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      x[r] = sc[r] * a.scale_log2;
+      if (tail && pg * P + 4 * grp + r >= t1) x[r] = kNegInf;
+    }
+    float mp = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mp = fmaxf(mp, __shfl_xor(mp, 16));
+    mp = fmaxf(mp, __shfl_xor(mp, 32));
+    if (__builtin_amdgcn_ballot_w64(mp > m)) {  // rescale only when a running max grows
+      if (mp > m) {
+        const float alpha = ex2(m - mp);
+        l *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 16; ++db) acc[db] *= alpha;
+        m = mp;
+      }
+    }
+    // P enters the product as fp16 hi + lo parts (p - hi is exact in fp32 and its fp16
+    // rounding leaves ~2^-22 relative), so P.V keeps the fp32 weights' accuracy
+    const float mref = (m == kNegInf) ? 0.0f : m;
+    h4v ph, pl;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float p = ex2(x[r] - mref);
+      l += p;
+      ph[r] = (_Float16)p;
+      pl[r] = (_Float16)(p - (float)ph[r]);
+    }
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) {
+      const h4v va = __builtin_bit_cast(h4v, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (lds_s4v*)((__attribute__((address_space(3))) char*)vst + tr_off + db * 32)));
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph, acc[db], 0, 0, 0);
+      acc[db] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, pl, acc[db], 0, 0, 0);
+    }
+  };
+
+  v4u ka[4], va[4], kb2[4], vb2[4];
+  for (int k0 = 0; k0 < npw; k0 += 64) {
+    const int n = min(64, npw - k0);
+    ids = (k0 + lane < npw) ? bt[first + (k0 + lane) * W] : 0;
+    issue(ka, va, 0);
+    int j = 0;
+    for (; j + 2 < n; j += 2) {
+      issue(kb2, vb2, j + 1);
+      consume(ka, va, k0 + j);
+      issue(ka, va, j + 2);
+      consume(kb2, vb2, k0 + j + 1);
+    }
+    if (j + 1 < n) {
+      issue(kb2, vb2, j + 1);
+      consume(ka, va, k0 + j);
+      consume(kb2, vb2, k0 + j + 1);
+    } else {
+      consume(ka, va, k0 + j);
+    }
+  }
+
+  // wave state: m per head (shared by the groups), l summed over the groups, acc
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  if (col < G) {
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db)
+      *reinterpret_cast<v4f*>(lds_acc + ((size_t)wave * G + col) * D + 16 * db + 4 * grp) = acc[db];
+    if (grp == 0) {
+      lds_m[wave * G + col] = m;
+      lds_l[wave * G + col] = l;
+    }
+  }
+  if (lane == 0) lds_bad[wave] = bad ? 1 : 0;
+  __syncthreads();
+  finish_task<G, W, COHERENT>(a, slot, lds);
+}
+
+// The task body each route runs: matrix-core products for G = 4 and 8, VALU otherwise.
+template <int G, int W, bool COHERENT>
+__device__ __forceinline__ void run_split_task(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
+                                               float* lds) {
+  if constexpr (mfma_task<G>())
+    run_task_mfma<G, W, COHERENT>(a, row, g, t0, t1, slot, lds);
+  else
+    run_task<G, W, COHERENT>(a, row, g, t0, t1, slot, lds);
 }
 
 template <int G>
@@ -978,7 +1180,7 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
       continue;
     }
-    run_task<G, W, FUSED>(a, row, g, t0, t1, t, lds);
+    run_split_task<G, W, FUSED>(a, row, g, t0, t1, t, lds);
     if (FUSED) {
       const int off = uniform(PLAN ? PL.off[row] : a.split_offsets[row]);
       int nsplit = uniform(PLAN ? PL.off[row + 1] : a.split_offsets[row + 1]) - off;
@@ -1042,7 +1244,7 @@ __global__ __launch_bounds__(W * 64) void rect_kernel(DecodeArgs a) {
   const int b1 = split_bound(s + 1, tiles, ns);
   const int t0 = b0 * T;
   const int t1 = min(b1 * T, n);
-  run_task<G, W, false>(a, row, g, t0, t1, slot, lds);
+  run_split_task<G, W, false>(a, row, g, t0, t1, slot, lds);
 }
 
 // Segmented merge: one workgroup per (row, KV head), the same merge_group code as the
