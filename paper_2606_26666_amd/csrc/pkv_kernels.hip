@@ -820,7 +820,7 @@ struct PlanLds {
   int* wmax;       // [NT / 64]
 };
 
-constexpr int kCandidateRows = 16;  // batches up to this size search the quota 64-wide
+constexpr int kCandidateRows = 16;  // batches up to this size test several quotas per step
 
 // Steps 1-3 for a batch of at most 64 rows and no block-table check: lane i of wave 0
 // holds row i, every batch quantity is a wave reduction and split_offsets a wave scan,
@@ -862,36 +862,30 @@ __device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanL
     auto nsplit_of = [&](int t, int q) { return t > 0 ? min(a.split_max, (t - 1) / q + 1) : 0; };
     int lo = 1;
     if (B <= kCandidateRows) {
-      // 64-way search: lane j tests the quota lo + (j + 1) * step - 1 over every row; the
-      // first fitting candidate narrows [lo, hi] to one step (the count only falls as the
-      // quota grows)
+      // R = B rounded up to a power of two; lane (c, i) = (lane / R, lane % R) counts row
+      // i's splits at the c-th of 64 / R candidate quotas lo + (c + 1) * step - 1, DPP
+      // row shifts sum each aligned group of R lanes into its last lane, and the first
+      // candidate that fits narrows [lo, hi] to one step (the count only falls as the
+      // quota grows). Rows live in lanes 0..15.
+      const int R = B <= 1 ? 1 : (B <= 2 ? 2 : (B <= 4 ? 4 : (B <= 8 ? 8 : 16)));
+      const int shift = R == 1 ? 0 : (R == 2 ? 1 : (R == 4 ? 2 : (R == 8 ? 3 : 4)));
+      const int ncand = 64 >> shift;
+      const int ti = __shfl(tiles, lane & (R - 1));
+      const int c = lane >> shift;
       while (lo < hi) {
-        const int step = (hi - lo + 64) >> 6;
-        const int q = min(hi, lo + (lane + 1) * step - 1);
-        const float rq = __builtin_amdgcn_rcpf((float)q);
-        int c = 0;
-        for (int i = 0; i < B; ++i) {
-          const int t = __builtin_amdgcn_readlane(tiles, i);
-          if (t <= 0) continue;
-          // ceil(t / q) = floor((t - 1) / q) + 1. Below 2^22 the float quotient is within
-          // one of the exact one (operand exact, reciprocal and product each within
-          // 2^-23 relative), so one integer correction step makes it exact.
-          int f;
-          if (t <= (1 << 22)) {
-            f = (int)((float)(t - 1) * rq);
-            const int rem = (t - 1) - f * q;
-            f += (rem >= q) - (rem < 0);
-          } else {
-            f = (t - 1) / q;
-          }
-          c += min(a.split_max, f + 1);
-        }
-        const unsigned long long fit = __ballot(c <= per_head);
+        const int step = (hi - lo + ncand) / ncand;
+        const int q = min(hi, lo + (c + 1) * step - 1);
+        int f = ti > 0 ? min(a.split_max, (ti - 1) / q + 1) : 0;
+        if (R > 1) f += dpp_i32<0x111>(f);  // row_shr:1
+        if (R > 2) f += dpp_i32<0x112>(f);  // row_shr:2
+        if (R > 4) f += dpp_i32<0x114>(f);  // row_shr:4
+        if (R > 8) f += dpp_i32<0x118>(f);  // row_shr:8
+        const unsigned long long fit = __ballot((lane & (R - 1)) == R - 1 && f <= per_head);
         if (fit == 0) {  // nothing up to hi fits: one split per row
           lo = hi;
           break;
         }
-        const int j = __ffsll((unsigned long long)fit) - 1;
+        const int j = (__ffsll((unsigned long long)fit) - 1) >> shift;
         const int qj = min(hi, lo + (j + 1) * step - 1);
         if (j > 0) lo = min(hi, lo + j * step - 1) + 1;
         hi = qj;
