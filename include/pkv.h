@@ -174,6 +174,10 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
  * checked by the decode (not by the planner), B <= 1024, params->num_kv_heads == Hkv.
  * The completion counters must be zero at launch: pkv_workspace_init zeroes them and
  * every completed pkv_plan, pkv_decode or pkv_plan_decode call leaves them zero.
+ * The previous contents of `tasks` (for B <= 64) are read as a scheduling hint: each
+ * workgroup starts loading the task listed at its own index while the planner runs and
+ * keeps those loads only if the new plan gives it the same pages. Any contents are
+ * allowed (out-of-range records are ignored) and never change a result.
  * Outputs are bit-identical to the two-call sequence. */
 int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
                     int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,

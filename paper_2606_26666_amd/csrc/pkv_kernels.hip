@@ -352,57 +352,60 @@ __device__ __forceinline__ void finish_task(const DecodeArgs& a, int slot, float
   }
 }
 
-template <int G, int W, bool COHERENT>
-__device__ __forceinline__ void run_task(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
-                                         float* lds) {
-  float* lds_m = lds;                // [W][G]
-  float* lds_l = lds + W * G;        // [W][G]
-  float* lds_acc = lds + 2 * W * G;  // [W][G][D]
-  int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
-
-  const int lane = threadIdx.x & 63;
-  const int wave = uniform(threadIdx.x >> 6);
-  const int r = lane >> 4;
-  const int c = lane & 15;
-  const int Hkv = a.Hkv;
-  const size_t tok_stride = (size_t)Hkv * D;       // halves between consecutive tokens
-  const size_t page_stride = (size_t)P * tok_stride;
-
+// A task body runs in three phases, so that the one-launch route can issue a task's
+// first loads before its plan is known (split_kernel):
+//   begin(row, g, t0, t1)  loads Q and the wave's first 64 page ids
+//   prime()                issues the loads of the wave's first two pages (waits for the ids)
+//   run(t1, slot)          the page loop, then the task's partial state into `slot`
+// covers(row, g, t0, t1) tells whether a begun task read exactly what task (row, g, t0,
+// t1) reads in those phases: the same row, head and first token and the same page
+// count. t1 itself only masks tokens of the last page, which run() applies.
+template <int G, int W>
+struct ValuTask {
+  int row = 0, g = 0, t0 = 0, pg_end = 0, first = 0, npw = 0, ids = 0;  // npw = 0: no task begun
+  bool bad = false;
   uint4 q[G];
-  {
-    const uint4* qp = reinterpret_cast<const uint4*>(a.q + ((size_t)row * a.Hq + (size_t)g * G) * D) + c;
+  uint4 ka[4], va[4], kb[4], vb[4];  // two pages in ping-pong
+
+  __device__ __forceinline__ void begin(const DecodeArgs& a, int row_, int g_, int t0_, int t1_) {
+    row = row_;
+    g = g_;
+    t0 = t0_;
+    pg_end = uniform((t1_ + P - 1) / P);
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform(threadIdx.x >> 6);
+    first = uniform(t0 / P + wave);  // this wave's pages: first + k*W
+    npw = uniform(first < pg_end ? (pg_end - first + W - 1) / W : 0);
+    bad = false;
+    const uint4* qp = reinterpret_cast<const uint4*>(a.q + ((size_t)row * a.Hq + (size_t)g * G) * D) + (lane & 15);
 #pragma unroll
     for (int h = 0; h < G; ++h) q[h] = qp[h * (D / 8)];
-  }
-  float m[G], l[G], acc[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m[h] = kNegInf;
-    l[h] = 0.0f;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) acc[h][k] = 0.0f;
+    ids = lane < npw ? a.block_table[(size_t)row * a.max_pages_per_row + first + lane * W] : 0;
   }
 
-  const int pg_begin = t0 / P;
-  const int pg_end = (t1 + P - 1) / P;
-  const int* bt = a.block_table + (size_t)row * a.max_pages_per_row;
-  // byte offsets inside one page: this lane's 16 bytes of token r, and 4 tokens further
-  const int lane_off_b = (int)(((size_t)r * tok_stride + (size_t)g * D + (size_t)c * 8) * 2);
-  const int step_b = (int)(4 * tok_stride * 2);
-  const int page_bytes = (int)(page_stride * 2);
-  const int first = pg_begin + wave;                       // this wave's pages: first + k*W
-  const int npw = first < pg_end ? (pg_end - first + W - 1) / W : 0;
-  bool bad = false;
+  __device__ __forceinline__ bool covers(int row_, int g_, int t0_, int t1_) const {
+    return row_ == row && g_ == g && t0_ == t0 && (t1_ + P - 1) / P == pg_end;
+  }
 
-  // Page ids of this wave's pages, 64 at a time, one per lane, fetched with one load and
-  // read back with v_readlane.
-  int ids = 0;
-  auto issue = [&](uint4 (&kr)[4], uint4 (&vr)[4], int j) {
-    int phys = __builtin_amdgcn_readlane(ids, j);
-    if (phys < 0 || phys >= a.num_pages) {
-      bad = true;
-      phys = 0;
-    }
+  // Page ids of this wave's pages sit 64 at a time in `ids`, one per lane, and are read
+  // back with v_readlane. Loads of the page in lane j of the id block into (kr, vr); a
+  // page that is not `live` is read through an empty descriptor, which returns zeros
+  // without touching memory, so the issue is branch-free.
+  __device__ __forceinline__ void issue(const DecodeArgs& a, uint4 (&kr)[4], uint4 (&vr)[4], int j, bool live) {
+    issue_page(a, kr, vr, __builtin_amdgcn_readlane(ids, j), live);
+  }
+  __device__ __forceinline__ void issue_page(const DecodeArgs& a, uint4 (&kr)[4], uint4 (&vr)[4], int phys,
+                                             bool live) {
+    const int lane = threadIdx.x & 63;
+    const size_t tok_stride = (size_t)a.Hkv * D;  // halves between consecutive tokens
+    const size_t page_stride = (size_t)P * tok_stride;
+    // byte offsets inside one page: this lane's 16 bytes of token r, and 4 tokens further
+    const int lane_off_b = (int)(((size_t)(lane >> 4) * tok_stride + (size_t)g * D + (size_t)(lane & 15) * 8) * 2);
+    const int step_b = (int)(4 * tok_stride * 2);
+    const bool ok = phys >= 0 && phys < a.num_pages;
+    bad |= live && !ok;
+    const int page_bytes = uniform(live ? (int)(page_stride * 2) : 0);
+    phys = uniform(live && ok ? phys : 0);
     // one buffer descriptor per page (scalar registers); lanes add their 32-bit offset
     const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, page_bytes);
     const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, page_bytes);
@@ -410,125 +413,154 @@ __device__ __forceinline__ void run_task(const DecodeArgs& a, int row, int g, in
     for (int i = 0; i < 4; ++i) kr[i] = buffer_load16(kr_rsrc, lane_off_b, i * step_b);
 #pragma unroll
     for (int i = 0; i < 4; ++i) vr[i] = buffer_load16(vr_rsrc, lane_off_b, i * step_b);
-  };
-  auto consume = [&](uint4 (&kr)[4], uint4 (&vr)[4], int k) {
-    const int pg = first + k * W;
-    float x[G][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int h = 0; h < G; ++h) x[h][i] = row_sum16(dot8(q[h], kr[i])) * a.scale_log2;
-    }
-    if (pg * P + P > t1) {  // the row's last, partial page: mask tokens >= t1
-      const int tok = pg * P + r;  // this lane row's token in load i is tok + 4i
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool valid = tok + 4 * i < t1;
-#pragma unroll
-        for (int h = 0; h < G; ++h) x[h][i] = valid ? x[h][i] : kNegInf;
-        if (!valid) vr[i] = make_uint4(0, 0, 0, 0);
-      }
-    }
-    float mt[G];
-    bool grow = false;
+  }
+
+  // Both issues are unconditional (pages past the wave's count are not live), so every
+  // path out of prime() has waited for the id load and issued the same loads, and the
+  // page loop's wait counts stay exact.
+  __device__ __forceinline__ void prime(const DecodeArgs& a) {
+    issue(a, ka, va, 0, npw > 0);
+    issue(a, kb, vb, 1, npw > 1);
+  }
+
+  template <bool COHERENT>
+  __device__ __forceinline__ void run(const DecodeArgs& a, int t1, int slot, float* lds) {
+    float* lds_m = lds;                // [W][G]
+    float* lds_l = lds + W * G;        // [W][G]
+    float* lds_acc = lds + 2 * W * G;  // [W][G][D]
+    int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform(threadIdx.x >> 6);
+    const int r = lane >> 4;
+    const int c = lane & 15;
+
+    float m[G], l[G], acc[G][8];
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      mt[h] = fmaxf(fmaxf(x[h][0], x[h][1]), fmaxf(x[h][2], x[h][3]));
-      grow |= mt[h] > m[h];
+      m[h] = kNegInf;
+      l[h] = 0.0f;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[h][k] = 0.0f;
     }
-    if (__builtin_amdgcn_ballot_w64(grow)) {  // rescale only when some running max grows
+
+    auto consume = [&](uint4 (&kr)[4], uint4 (&vr)[4], int k) {
+      const int pg = first + k * W;
+      float x[G][4];
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        if (mt[h] > m[h]) {
-          const float alpha = ex2(m[h] - mt[h]);
-          l[h] *= alpha;
+      for (int i = 0; i < 4; ++i) {
 #pragma unroll
-          for (int kk = 0; kk < 8; ++kk) acc[h][kk] *= alpha;
-          m[h] = mt[h];
+        for (int h = 0; h < G; ++h) x[h][i] = row_sum16(dot8(q[h], kr[i])) * a.scale_log2;
+      }
+      if (pg * P + P > t1) {  // the row's last, partial page: mask tokens >= t1
+        const int tok = pg * P + r;  // this lane row's token in load i is tok + 4i
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool valid = tok + 4 * i < t1;
+#pragma unroll
+          for (int h = 0; h < G; ++h) x[h][i] = valid ? x[h][i] : kNegInf;
+          if (!valid) vr[i] = make_uint4(0, 0, 0, 0);
         }
       }
+      float mt[G];
+      bool grow = false;
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        mt[h] = fmaxf(fmaxf(x[h][0], x[h][1]), fmaxf(x[h][2], x[h][3]));
+        grow |= mt[h] > m[h];
+      }
+      if (__builtin_amdgcn_ballot_w64(grow)) {  // rescale only when some running max grows
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          if (mt[h] > m[h]) {
+            const float alpha = ex2(m[h] - mt[h]);
+            l[h] *= alpha;
+#pragma unroll
+            for (int kk = 0; kk < 8; ++kk) acc[h][kk] *= alpha;
+            m[h] = mt[h];
+          }
+        }
+      }
+      float vf[4][8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) unpack8(vr[i], vf[i]);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float mref = (m[h] == kNegInf) ? 0.0f : m[h];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p = ex2(x[h][i] - mref);
+          l[h] += p;
+#pragma unroll
+          for (int kk = 0; kk < 8; ++kk) acc[h][kk] = __builtin_fmaf(p, vf[i][kk], acc[h][kk]);
+        }
+      }
+    };
+
+    // Two register buffers in ping-pong: the next page's loads are in flight while the
+    // current page is scored and accumulated. Inside the steady-state loop every load is
+    // unconditional, so each consume waits only for its own buffer's loads. begin() and
+    // prime() have fetched the first id block and issued the first two pages.
+    for (int k0 = 0; k0 < npw; k0 += 64) {
+      const int n = min(64, npw - k0);
+      if (k0 > 0) {  // begin() and prime() did this for the first id block
+        ids = (k0 + lane < npw) ? a.block_table[(size_t)row * a.max_pages_per_row + first + (k0 + lane) * W] : 0;
+        issue(a, ka, va, 0, true);
+        issue(a, kb, vb, 1, n > 1);
+      }
+      // pages j (ka) and j + 1 (kb) are in flight at the top of each iteration
+      int j = 0;
+      for (; j + 2 < n; j += 2) {
+        consume(ka, va, k0 + j);
+        issue(a, ka, va, j + 2, true);
+        consume(kb, vb, k0 + j + 1);
+        issue(a, kb, vb, (j + 3) & 63, j + 3 < n);
+      }
+      consume(ka, va, k0 + j);
+      if (j + 1 < n) consume(kb, vb, k0 + j + 1);
     }
-    float vf[4][8];
+
+    // Combine the wave's four lane rows (butterfly over lane xor 16, then xor 32); the
+    // lanes of row 0 then hold the wave's state, which goes to LDS for a fixed-order
+    // combine of the W wave states into the task's partial state.
 #pragma unroll
-    for (int i = 0; i < 4; ++i) unpack8(vr[i], vf[i]);
+    for (int sh = 16; sh <= 32; sh <<= 1) {
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mref = (m[h] == kNegInf) ? 0.0f : m[h];
+      for (int h = 0; h < G; ++h) {
+        const float mo = __shfl_xor(m[h], sh);
+        const float lo = __shfl_xor(l[h], sh);
+        const float M = fmaxf(m[h], mo);
+        const float Mref = (M == kNegInf) ? 0.0f : M;
+        const float ca = ex2(m[h] - Mref);
+        const float cb = ex2(mo - Mref);
+        l[h] = __builtin_fmaf(cb, lo, ca * l[h]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = ex2(x[h][i] - mref);
-        l[h] += p;
-#pragma unroll
-        for (int kk = 0; kk < 8; ++kk) acc[h][kk] = __builtin_fmaf(p, vf[i][kk], acc[h][kk]);
+        for (int k = 0; k < 8; ++k) {
+          const float ao = __shfl_xor(acc[h][k], sh);
+          acc[h][k] = __builtin_fmaf(cb, ao, ca * acc[h][k]);
+        }
+        m[h] = M;
       }
     }
-  };
-
-  // Two register buffers in ping-pong: the next page's loads are in flight while the
-  // current page is scored and accumulated. Inside the steady-state loop every load is
-  // unconditional, so each consume waits only for its own buffer's loads.
-  uint4 ka[4], va[4], kb2[4], vb2[4];
-  for (int k0 = 0; k0 < npw; k0 += 64) {
-    const int n = min(64, npw - k0);
-    ids = (k0 + lane < npw) ? bt[first + (k0 + lane) * W] : 0;
-    issue(ka, va, 0);
-    int j = 0;
-    for (; j + 2 < n; j += 2) {
-      issue(kb2, vb2, j + 1);
-      consume(ka, va, k0 + j);
-      issue(ka, va, j + 2);
-      consume(kb2, vb2, k0 + j + 1);
-    }
-    if (j + 1 < n) {
-      issue(kb2, vb2, j + 1);
-      consume(ka, va, k0 + j);
-      consume(kb2, vb2, k0 + j + 1);
-    } else {
-      consume(ka, va, k0 + j);
-    }
-  }
-
-  // Combine the wave's four lane rows (butterfly over lane xor 16, then xor 32); the
-  // lanes of row 0 then hold the wave's state, which goes to LDS for a fixed-order
-  // combine of the W wave states into the task's partial state.
+    if (lane < 16) {
 #pragma unroll
-  for (int sh = 16; sh <= 32; sh <<= 1) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float mo = __shfl_xor(m[h], sh);
-      const float lo = __shfl_xor(l[h], sh);
-      const float M = fmaxf(m[h], mo);
-      const float Mref = (M == kNegInf) ? 0.0f : M;
-      const float ca = ex2(m[h] - Mref);
-      const float cb = ex2(mo - Mref);
-      l[h] = __builtin_fmaf(cb, lo, ca * l[h]);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const float ao = __shfl_xor(acc[h][k], sh);
-        acc[h][k] = __builtin_fmaf(cb, ao, ca * acc[h][k]);
+      for (int h = 0; h < G; ++h) {
+        float4* dst = reinterpret_cast<float4*>(lds_acc + ((size_t)wave * G + h) * D + c * 8);
+        dst[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
+        dst[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
       }
-      m[h] = M;
     }
-  }
-  if (lane < 16) {
+    if (lane == 0) {
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float4* dst = reinterpret_cast<float4*>(lds_acc + ((size_t)wave * G + h) * D + c * 8);
-      dst[0] = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
-      dst[1] = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
+      for (int h = 0; h < G; ++h) {
+        lds_m[wave * G + h] = m[h];
+        lds_l[wave * G + h] = l[h];
+      }
+      lds_bad[wave] = bad ? 1 : 0;
     }
+    __syncthreads();
+    finish_task<G, W, COHERENT>(a, slot, lds);
   }
-  if (lane == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      lds_m[wave * G + h] = m[h];
-      lds_l[wave * G + h] = l[h];
-    }
-    lds_bad[wave] = bad ? 1 : 0;
-  }
-  __syncthreads();
-  finish_task<G, W, COHERENT>(a, slot, lds);
-}
+};
 
 // ---------------------------------------------------------------------------------
 // The same task with both products on the matrix cores (for G = 4 and 8, where the
@@ -559,28 +591,27 @@ constexpr bool mfma_task() {
   return G == 4 || G == 8;
 }
 
-template <int G, int W, bool COHERENT>
-__device__ __forceinline__ void run_task_mfma(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
-                                              float* lds) {
+// The phases and covers() are those of ValuTask.
+template <int G, int W>
+struct MfmaTask {
   static_assert(G <= 16, "heads fit the 16 MFMA columns");
-  __shared__ v4u vstage[W][P * D / 8];  // one V page of one head per wave: 16 rows of 256 B
-  float* lds_m = lds;                // [W][G]
-  float* lds_l = lds + W * G;        // [W][G]
-  float* lds_acc = lds + 2 * W * G;  // [W][G][D]
-  int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
-
-  const int lane = threadIdx.x & 63;
-  const int wave = uniform(threadIdx.x >> 6);
-  const int grp = lane >> 4;
-  const int col = lane & 15;
-  const int Hkv = a.Hkv;
-  const size_t tok_stride = (size_t)Hkv * D;  // halves between consecutive tokens
-  const size_t page_stride = (size_t)P * tok_stride;
-  const int tok_b = (int)(tok_stride * 2);
-  const int page_bytes = (int)(page_stride * 2);
-
+  int row = 0, g = 0, t0 = 0, pg_end = 0, first = 0, npw = 0, ids = 0;  // npw = 0: no task begun
+  bool bad = false;
   v4u qb[4];
-  {
+  v4u ka[4], va[4], kb[4], vb[4];
+
+  __device__ __forceinline__ void begin(const DecodeArgs& a, int row_, int g_, int t0_, int t1_) {
+    row = row_;
+    g = g_;
+    t0 = t0_;
+    pg_end = uniform((t1_ + P - 1) / P);
+    const int lane = threadIdx.x & 63;
+    const int grp = lane >> 4;
+    const int col = lane & 15;
+    const int wave = uniform(threadIdx.x >> 6);
+    first = uniform(t0 / P + wave);
+    npw = uniform(first < pg_end ? (pg_end - first + W - 1) / W : 0);
+    bad = false;
     const bool hv = col < G;
     const uint16_t* qh = a.q + ((size_t)row * a.Hq + (size_t)g * G + (hv ? col : 0)) * D;
 #pragma unroll
@@ -588,137 +619,173 @@ __device__ __forceinline__ void run_task_mfma(const DecodeArgs& a, int row, int 
       const v4u z = {0u, 0u, 0u, 0u};
       qb[kb] = hv ? *reinterpret_cast<const v4u*>(qh + kb * 32 + 8 * grp) : z;
     }
+    ids = lane < npw ? a.block_table[(size_t)row * a.max_pages_per_row + first + lane * W] : 0;
   }
-  float m = kNegInf, l = 0.0f;
-  v4f acc[D / 16];
-#pragma unroll
-  for (int db = 0; db < D / 16; ++db) acc[db] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 
-  const int pg_begin = t0 / P;
-  const int pg_end = (t1 + P - 1) / P;
-  const int* bt = a.block_table + (size_t)row * a.max_pages_per_row;
-  const int k_off = col * tok_b + g * D * 2 + grp * 16;  // + 64 kb
-  const int v_off = grp * tok_b + g * D * 2 + col * 16;  // + 4 i tok_b
-  const int v_step = 4 * tok_b;
-  const int first = pg_begin + wave;
-  const int npw = first < pg_end ? (pg_end - first + W - 1) / W : 0;
-  bool bad = false;
-  v4u* vst = &vstage[wave][0];
-  const int tr_off = (4 * grp + (col >> 2)) * (D * 2) + (col & 3) * 8;  // + 32 db
+  __device__ __forceinline__ bool covers(int row_, int g_, int t0_, int t1_) const {
+    return row_ == row && g_ == g && t0_ == t0 && (t1_ + P - 1) / P == pg_end;
+  }
 
-  int ids = 0;
-  auto issue = [&](v4u (&kr)[4], v4u (&vr)[4], int j) {
-    int phys = __builtin_amdgcn_readlane(ids, j);
-    if (phys < 0 || phys >= a.num_pages) {
-      bad = true;
-      phys = 0;
-    }
+  __device__ __forceinline__ void issue(const DecodeArgs& a, v4u (&kr)[4], v4u (&vr)[4], int j, bool live) {
+    issue_page(a, kr, vr, __builtin_amdgcn_readlane(ids, j), live);
+  }
+  __device__ __forceinline__ void issue_page(const DecodeArgs& a, v4u (&kr)[4], v4u (&vr)[4], int phys, bool live) {
+    const int lane = threadIdx.x & 63;
+    const int grp = lane >> 4;
+    const int col = lane & 15;
+    const size_t tok_stride = (size_t)a.Hkv * D;  // halves between consecutive tokens
+    const size_t page_stride = (size_t)P * tok_stride;
+    const int tok_b = (int)(tok_stride * 2);
+    const int k_off = col * tok_b + g * D * 2 + grp * 16;  // + 64 kb
+    const int v_off = grp * tok_b + g * D * 2 + col * 16;  // + 4 i tok_b
+    const bool ok = phys >= 0 && phys < a.num_pages;
+    bad |= live && !ok;
+    const int page_bytes = uniform(live ? (int)(page_stride * 2) : 0);
+    phys = uniform(live && ok ? phys : 0);
     const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, page_bytes);
     const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, page_bytes);
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) kr[kb] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, k_off, kb * 64, 0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, v_off, i * v_step, 0);
-  };
-  auto consume = [&](v4u (&kr)[4], v4u (&vr)[4], int k) {
-    const int pg = first + k * W;
-    const bool tail = pg * P + P > t1;  // the row's last, partial page
-    v4f sc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, v_off, i * 4 * tok_b, 0);
+  }
+
+  // Both issues are unconditional (pages past the wave's count are not live), so every
+  // path out of prime() has waited for the id load and issued the same loads, and the
+  // page loop's wait counts stay exact.
+  __device__ __forceinline__ void prime(const DecodeArgs& a) {
+    issue(a, ka, va, 0, npw > 0);
+    issue(a, kb, vb, 1, npw > 1);
+  }
+
+  template <bool COHERENT>
+  __device__ __forceinline__ void run(const DecodeArgs& a, int t1, int slot, float* lds) {
+    __shared__ v4u vstage[W][P * D / 8];  // one V page of one head per wave: 16 rows of 256 B
+    float* lds_m = lds;                // [W][G]
+    float* lds_l = lds + W * G;        // [W][G]
+    float* lds_acc = lds + 2 * W * G;  // [W][G][D]
+    int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
+    const int lane = threadIdx.x & 63;
+    const int wave = uniform(threadIdx.x >> 6);
+    const int grp = lane >> 4;
+    const int col = lane & 15;
+
+    float m = kNegInf, l = 0.0f;
+    v4f acc[D / 16];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[kb]), __builtin_bit_cast(h8v, qb[kb]),
-                                                  sc, 0, 0, 0);
-    // stage V token-major; rows past t1 are zeroed (their p is 0, but 0 * NaN is not)
+    for (int db = 0; db < D / 16; ++db) acc[db] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    v4u* vst = &vstage[wave][0];
+    const int tr_off = (4 * grp + (col >> 2)) * (D * 2) + (col & 3) * 8;  // + 32 db
+
+    auto consume = [&](v4u (&kr)[4], v4u (&vr)[4], int k) {
+      const int pg = first + k * W;
+      const bool tail = pg * P + P > t1;  // the row's last, partial page
+      v4f sc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v4u v = vr[i];
-      if (tail && pg * P + 4 * i + grp >= t1) v = v4u{0u, 0u, 0u, 0u};
-      vst[(4 * i + grp) * (D / 8) + col] = v;
+      for (int kb = 0; kb < 4; ++kb)
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[kb]), __builtin_bit_cast(h8v, qb[kb]),
+                                                    sc, 0, 0, 0);
+      // stage V token-major; rows past t1 are zeroed (their p is 0, but 0 * NaN is not)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v4u v = vr[i];
+        if (tail && pg * P + 4 * i + grp >= t1) v = v4u{0u, 0u, 0u, 0u};
+        vst[(4 * i + grp) * (D / 8) + col] = v;
+      }
+      float x[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        x[r] = sc[r] * a.scale_log2;
+        if (tail && pg * P + 4 * grp + r >= t1) x[r] = kNegInf;
+      }
+      float mp = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      mp = fmaxf(mp, __shfl_xor(mp, 16));
+      mp = fmaxf(mp, __shfl_xor(mp, 32));
+      if (__builtin_amdgcn_ballot_w64(mp > m)) {  // rescale only when a running max grows
+        if (mp > m) {
+          const float alpha = ex2(m - mp);
+          l *= alpha;
+#pragma unroll
+          for (int db = 0; db < D / 16; ++db) acc[db] *= alpha;
+          m = mp;
+        }
+      }
+      // P enters the product as fp16 hi + lo parts (p - hi is exact in fp32 and its fp16
+      // rounding leaves ~2^-22 relative), so P.V keeps the fp32 weights' accuracy
+      const float mref = (m == kNegInf) ? 0.0f : m;
+      h4v ph, pl;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float p = ex2(x[r] - mref);
+        l += p;
+        ph[r] = (_Float16)p;
+        pl[r] = (_Float16)(p - (float)ph[r]);
+      }
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) {
+        const h4v va_ = __builtin_bit_cast(h4v, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s4v*)((__attribute__((address_space(3))) char*)vst + tr_off + db * 32)));
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x16f16(va_, ph, acc[db], 0, 0, 0);
+        acc[db] = __builtin_amdgcn_mfma_f32_16x16x16f16(va_, pl, acc[db], 0, 0, 0);
+      }
+    };
+
+    for (int k0 = 0; k0 < npw; k0 += 64) {
+      const int n = min(64, npw - k0);
+      if (k0 > 0) {  // begin() and prime() did this for the first id block
+        ids = (k0 + lane < npw) ? a.block_table[(size_t)row * a.max_pages_per_row + first + (k0 + lane) * W] : 0;
+        issue(a, ka, va, 0, true);
+        issue(a, kb, vb, 1, n > 1);
+      }
+      // pages j (ka) and j + 1 (kb) are in flight at the top of each iteration
+      int j = 0;
+      for (; j + 2 < n; j += 2) {
+        consume(ka, va, k0 + j);
+        issue(a, ka, va, j + 2, true);
+        consume(kb, vb, k0 + j + 1);
+        issue(a, kb, vb, (j + 3) & 63, j + 3 < n);
+      }
+      consume(ka, va, k0 + j);
+      if (j + 1 < n) consume(kb, vb, k0 + j + 1);
     }
-    float x[4];
+
+    // wave state: m per head (shared by the groups), l summed over the groups, acc
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    if (col < G) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      x[r] = sc[r] * a.scale_log2;
-      if (tail && pg * P + 4 * grp + r >= t1) x[r] = kNegInf;
-    }
-    float mp = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mp = fmaxf(mp, __shfl_xor(mp, 16));
-    mp = fmaxf(mp, __shfl_xor(mp, 32));
-    if (__builtin_amdgcn_ballot_w64(mp > m)) {  // rescale only when a running max grows
-      if (mp > m) {
-        const float alpha = ex2(m - mp);
-        l *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 16; ++db) acc[db] *= alpha;
-        m = mp;
+      for (int db = 0; db < D / 16; ++db)
+        *reinterpret_cast<v4f*>(lds_acc + ((size_t)wave * G + col) * D + 16 * db + 4 * grp) = acc[db];
+      if (grp == 0) {
+        lds_m[wave * G + col] = m;
+        lds_l[wave * G + col] = l;
       }
     }
-    // P enters the product as fp16 hi + lo parts (p - hi is exact in fp32 and its fp16
-    // rounding leaves ~2^-22 relative), so P.V keeps the fp32 weights' accuracy
-    const float mref = (m == kNegInf) ? 0.0f : m;
-    h4v ph, pl;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float p = ex2(x[r] - mref);
-      l += p;
-      ph[r] = (_Float16)p;
-      pl[r] = (_Float16)(p - (float)ph[r]);
-    }
-#pragma unroll
-    for (int db = 0; db < D / 16; ++db) {
-      const h4v va = __builtin_bit_cast(h4v, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (lds_s4v*)((__attribute__((address_space(3))) char*)vst + tr_off + db * 32)));
-      acc[db] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph, acc[db], 0, 0, 0);
-      acc[db] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, pl, acc[db], 0, 0, 0);
-    }
-  };
-
-  v4u ka[4], va[4], kb2[4], vb2[4];
-  for (int k0 = 0; k0 < npw; k0 += 64) {
-    const int n = min(64, npw - k0);
-    ids = (k0 + lane < npw) ? bt[first + (k0 + lane) * W] : 0;
-    issue(ka, va, 0);
-    int j = 0;
-    for (; j + 2 < n; j += 2) {
-      issue(kb2, vb2, j + 1);
-      consume(ka, va, k0 + j);
-      issue(ka, va, j + 2);
-      consume(kb2, vb2, k0 + j + 1);
-    }
-    if (j + 1 < n) {
-      issue(kb2, vb2, j + 1);
-      consume(ka, va, k0 + j);
-      consume(kb2, vb2, k0 + j + 1);
-    } else {
-      consume(ka, va, k0 + j);
-    }
+    if (lane == 0) lds_bad[wave] = bad ? 1 : 0;
+    __syncthreads();
+    finish_task<G, W, COHERENT>(a, slot, lds);
   }
-
-  // wave state: m per head (shared by the groups), l summed over the groups, acc
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-  if (col < G) {
-#pragma unroll
-    for (int db = 0; db < D / 16; ++db)
-      *reinterpret_cast<v4f*>(lds_acc + ((size_t)wave * G + col) * D + 16 * db + 4 * grp) = acc[db];
-    if (grp == 0) {
-      lds_m[wave * G + col] = m;
-      lds_l[wave * G + col] = l;
-    }
-  }
-  if (lane == 0) lds_bad[wave] = bad ? 1 : 0;
-  __syncthreads();
-  finish_task<G, W, COHERENT>(a, slot, lds);
-}
+};
 
 // The task body each route runs: matrix-core products for G = 4 and 8, VALU otherwise.
+template <bool MFMA, int G, int W>
+struct BodySel {
+  using type = ValuTask<G, W>;
+};
+template <int G, int W>
+struct BodySel<true, G, W> {
+  using type = MfmaTask<G, W>;
+};
+template <int G, int W>
+using TaskBody = typename BodySel<mfma_task<G>(), G, W>::type;
+
 template <int G, int W, bool COHERENT>
 __device__ __forceinline__ void run_split_task(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
                                                float* lds) {
-  if constexpr (mfma_task<G>())
-    run_task_mfma<G, W, COHERENT>(a, row, g, t0, t1, slot, lds);
-  else
-    run_task<G, W, COHERENT>(a, row, g, t0, t1, slot, lds);
+  TaskBody<G, W> body;
+  body.begin(a, row, g, t0, t1);
+  body.prime(a);
+  body.template run<COHERENT>(a, t1, slot, lds);
 }
 
 template <int G>
@@ -825,12 +892,19 @@ constexpr int kCandidateRows = 16;  // batches up to this size test several quot
 // Steps 1-3 for a batch of at most 64 rows and no block-table check: lane i of wave 0
 // holds row i, every batch quantity is a wave reduction and split_offsets a wave scan,
 // so the workgroup meets a single barrier. Same results as the general path below.
-__device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanLds& L, bool report) {
+// `n` is seq_lens[lane] (0 for lanes >= B), loaded by the caller.
+__device__ __forceinline__ bool wave_plan(const PlanArgs& a) { return a.B <= 64 && !a.block_table; }
+
+__device__ __forceinline__ int wave_plan_len(const PlanArgs& a) {
+  const int lane = threadIdx.x & 63;
+  return lane < a.B ? a.seq_lens[lane] : 0;
+}
+
+__device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanLds& L, bool report, int n) {
   const int lane = threadIdx.x & 63;
   const int B = a.B;
   const int T = a.tile_tokens;
   const int cap = a.max_pages_per_row * a.page_size;
-  int n = lane < B ? a.seq_lens[lane] : 0;
   if (n < 0 || n > cap) {
     if (report) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
     n = 0;
@@ -908,17 +982,22 @@ __device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanL
 
 // Steps 1-3: validated lengths in L.len, split_offsets in L.off; returns the task count
 // (every thread). `report` selects the workgroup that raises device error bits.
+// Task count of a plan formed by plan_compute_wave (after the workgroup barrier).
+__device__ __forceinline__ int plan_wave_tasks(const PlanArgs& a, const PlanLds& L, bool report) {
+  long long nt = (long long)L.off[a.B] * a.Hkv;
+  if (nt > a.max_tasks) {  // excluded by host validation; never write past the buffer
+    if (report && threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
+    nt = 0;
+  }
+  return (int)nt;
+}
+
 template <int NT>
 __device__ __forceinline__ int plan_compute(const PlanArgs& a, const PlanLds& L, bool report) {
-  if (a.B <= 64 && !a.block_table) {
-    if (threadIdx.x < 64) plan_compute_wave(a, L, report);
+  if (wave_plan(a)) {
+    if (threadIdx.x < 64) plan_compute_wave(a, L, report, wave_plan_len(a));
     __syncthreads();
-    long long nt = (long long)L.off[a.B] * a.Hkv;
-    if (nt > a.max_tasks) {  // excluded by host validation; never write past the buffer
-      if (report && threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_SEQ_LEN);
-      nt = 0;
-    }
-    return (int)nt;
+    return plan_wave_tasks(a, L, report);
   }
   constexpr int NW = NT / 64;
   const int tid = threadIdx.x;
@@ -1139,10 +1218,38 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   // the start, so later scalar loads of them do not wait on memory (after the planner,
   // and at the end of the last task).
   asm volatile("" ::"s"(a.q), "s"(a.partials), "s"(gridDim.x));
+  TaskBody<G, W> body;
+  bool begun = false;  // this wave's body holds a task begun before the plan
   int plan_ntasks = 0;
   if (PLAN) {
-    plan_ntasks = plan_compute<W * 64>(a.plan, PL, blockIdx.x == 0);
-    if (blockIdx.x == 0) plan_write<W * 64, false>(a.plan, PL, plan_ntasks, false);
+    if (wave_plan(a.plan)) {
+      // Speculative start. Between decode steps a plan rarely changes (lengths grow by a
+      // token), so while the planner runs, each wave begins and primes the task listed
+      // at this workgroup's index in the task list left by the previous launch (the task
+      // it ran then): a hint, read with agent-scope loads because workgroup 0 rewrites
+      // the list meanwhile. A record
+      // is used only if it names a task inside the batch's bounds (the buffer may hold
+      // anything on the first call), and the begun loads are kept only if the new plan
+      // gives this workgroup a task they cover; otherwise the task is begun again. The
+      // results never depend on the hint.
+      const int n_raw = threadIdx.x < 64 ? wave_plan_len(a.plan) : 0;  // the planner's load goes first
+      if ((int)blockIdx.x < a.max_tasks) {
+        const int* tp = reinterpret_cast<const int*>(a.tasks + blockIdx.x);
+        const int hr = uniform(ld_i32<true>(tp + 0)), hg = uniform(ld_i32<true>(tp + 1));
+        const int h0 = uniform(ld_i32<true>(tp + 3)), h1 = uniform(ld_i32<true>(tp + 4));
+        if (hr >= 0 && hr < a.B && hg >= 0 && hg < a.Hkv && h0 >= 0 && h1 > h0 && h1 <= a.max_pages_per_row * P) {
+          body.begin(a, hr, hg, h0, h1);
+          begun = true;
+        }
+      }
+      if (threadIdx.x < 64) plan_compute_wave(a.plan, PL, blockIdx.x == 0, n_raw);
+      body.prime(a);  // nothing to issue when no task was begun (npw = 0)
+      __syncthreads();
+      plan_ntasks = plan_wave_tasks(a.plan, PL, blockIdx.x == 0);
+    } else {
+      plan_ntasks = plan_compute<W * 64>(a.plan, PL, blockIdx.x == 0);
+    }
+    if (blockIdx.x == 0) plan_write<W * 64, true>(a.plan, PL, plan_ntasks, false);
   }
   // The first task record is fetched together with the task count (the grid never
   // exceeds max_tasks, so the record lies inside the task buffer even when unused).
@@ -1174,7 +1281,12 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
       continue;
     }
-    run_split_task<G, W, FUSED>(a, row, g, t0, t1, t, lds);
+    if (!(begun && t == (int)blockIdx.x && body.covers(row, g, t0, t1))) {
+      body.begin(a, row, g, t0, t1);
+      body.prime(a);
+    }
+    begun = false;
+    body.template run<FUSED>(a, t1, t, lds);
     if (FUSED) {
       const int off = uniform(PLAN ? PL.off[row] : a.split_offsets[row]);
       int nsplit = uniform(PLAN ? PL.off[row + 1] : a.split_offsets[row + 1]) - off;

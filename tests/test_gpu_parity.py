@@ -347,3 +347,88 @@ def test_coarse_buckets_on_benchmark_config():
     assert launches == 2 * groups
     assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), "coarse buckets")
     assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+def _two_launch(case, p, split_max):
+    """Plan kernel, then the fused decode kernel: the route without a speculative start."""
+    bufs = bufs_for(case, split_max)
+    run_plan(case, bufs, p)
+    out = run_decode(case, bufs)
+    tasks, offs = read_plan(bufs)
+    return out, tasks, offs
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_plan_decode_hints_never_change_results(policy):
+    """The one-launch route starts each workgroup on the task that the previous call
+    listed at the workgroup's index. Whatever the task buffer holds (garbage, plausible
+    but wrong records, the right records at the wrong slots, the exact plan), outputs
+    and the task list are bitwise those of the route without that start."""
+    case = Case([900, 0, 17, 4096, 33, 2500, 1, 700], seed=21)
+    p = plan_params(8, 2, 16, 200, policy=policy)
+    expect, tasks_ref, offs_ref = _two_launch(case, p, 16)
+    assert np.array_equal(tasks_ref, oracle_plan(case, p)[0])
+    r = np.random.Generator(np.random.PCG64(5))
+    bufs = bufs_for(case, 16)
+    cap = bufs.tasks.shape[0]
+    maxp = case.bt.shape[1]
+    garbage = r.integers(-(1 << 30), 1 << 30, size=(cap, 5), dtype=np.int64).astype(np.int32)
+    plausible = np.zeros((cap, 5), dtype=np.int32)
+    plausible[:, 0] = r.integers(0, case.B, size=cap)
+    plausible[:, 1] = r.integers(0, 8, size=cap)
+    plausible[:, 3] = 16 * r.integers(0, maxp, size=cap)
+    plausible[:, 4] = np.minimum(plausible[:, 3] + r.integers(1, 600, size=cap), maxp * 16)
+    shuffled = np.zeros((cap, 5), dtype=np.int32)
+    shuffled[:len(tasks_ref)] = tasks_ref[r.permutation(len(tasks_ref))]
+    exact = np.zeros((cap, 5), dtype=np.int32)
+    exact[:len(tasks_ref)] = tasks_ref
+    for label, hint in [("garbage", garbage), ("plausible", plausible), ("shuffled", shuffled), ("exact", exact)]:
+        bufs.tasks.copy_(torch.from_numpy(hint).view(bufs.tasks.dtype).reshape(bufs.tasks.shape).cuda())
+        got = run_plan_decode(case, bufs, p)
+        tasks, offs = read_plan(bufs)
+        assert torch.equal(got, expect), label
+        assert np.array_equal(tasks, tasks_ref) and np.array_equal(offs, offs_ref), label
+        assert pkv.pkv_check_device_status(bufs.ws) == 0, label
+
+
+def test_plan_decode_speculation_across_growing_steps():
+    """Decode steps with every row one token longer than at the previous step (pages and
+    tiles fill and new ones start), one workspace throughout: each step's output is bitwise
+    that of the two-launch route, and its task list is the oracle's."""
+    base = np.array([1000, 15, 4063, 31, 300, 2047, 64, 9000], dtype=np.int32)
+    steps = 40
+    case = Case(base + steps, seed=22)
+    p = plan_params(8, 1, 64, 256, policy=1)
+    bufs = bufs_for(case, 64)
+    for s in range(steps + 1):
+        lens = base + s
+        case.lens = lens
+        case.lens_dev = torch.from_numpy(lens).cuda()
+        expect, tasks_ref, _ = _two_launch(case, p, 64)
+        got = run_plan_decode(case, bufs, p)
+        tasks, _ = read_plan(bufs)
+        assert torch.equal(got, expect), s
+        assert np.array_equal(tasks, tasks_ref), s
+        if s % 13 == 0:
+            assert np.array_equal(tasks, oracle_plan(case, p)[0]), s
+            assert_close(got, ref_decode(case.q, case.k, case.v, case.bt, lens), f"step {s}")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+def test_plan_decode_batch_above_one_wave():
+    """More than 64 rows: the one-launch route plans with the workgroup-wide planner and
+    starts no task early. Twice on one workspace."""
+    r = np.random.Generator(np.random.PCG64(23))
+    lens = r.integers(0, 700, size=80).astype(np.int32)
+    lens[::9] = 0
+    case = Case(lens, seed=23)
+    p = plan_params(8, 1, 4, 600, policy=1)
+    ref = ref_decode(case.q, case.k, case.v, case.bt, case.lens)
+    bufs = bufs_for(case, 4)
+    for rep in range(2):
+        out = run_plan_decode(case, bufs, p)
+        assert_close(out, ref, f"B=80 call {rep}")
+        tasks, offs = read_plan(bufs)
+        plan = oracle_plan(case, p)
+        assert np.array_equal(tasks, plan[0]) and np.array_equal(offs, plan[1]), rep
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
