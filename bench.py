@@ -29,6 +29,7 @@ cpu_baseline = the fp64 numpy oracle on the host over the same steps' inputs.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -83,7 +84,11 @@ class Runner:
         from workloads.values import device_normal_f16, q_values
 
         self.torch, self.pkv = torch, pkv
-        self.w = w = make_workload(name, seed=seed, steps=steps, target_tasks=target_tasks, hkv=hkv)
+        w = make_workload(name, seed=seed, steps=steps, hkv=hkv)
+        if not target_tasks:  # the cost model's rule for the first step's active rows
+            from paper_2606_26666_amd import costmodel
+            target_tasks = costmodel.default_target(int(np.count_nonzero(w.lengths_at(0))), w.hkv)
+        self.w = w = dataclasses.replace(w, target_tasks=target_tasks)
         self.dev = torch.device("cuda:0")
         shape = (w.num_pages, w.page_size, w.hkv, w.head_dim)
         self.k = device_normal_f16(shape, seed * 4 + 1, self.dev)
@@ -453,8 +458,9 @@ def main():
     ap.add_argument("--workload", default="b1")
     ap.add_argument("--also", default="b8_bimodal", help="comma-separated extra workloads, or 'none'")
     ap.add_argument("--seed", type=int, default=20260623)
-    ap.add_argument("--target-tasks", type=int, default=256,
-                    help="planner task target; 256 = one task per compute unit")
+    ap.add_argument("--target-tasks", type=int, default=0,
+                    help="planner task target; 0 = the cost model's rule, max(256, 4 * Hkv * active rows) "
+                         "(256 = one task per compute unit)")
     ap.add_argument("--policy", type=int, default=1,
                     help="split policy: 0 one split count from the active batch size, 1 tile quota (smallest "
                          "per-split tile quota whose task count fits --target-tasks)")

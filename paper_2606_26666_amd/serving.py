@@ -27,6 +27,7 @@ import time
 import numpy as np
 
 from . import _binding as _b
+from . import costmodel
 
 PAGE = 16
 
@@ -76,7 +77,7 @@ class Engine:
     token's K/V at the row's next position before attending."""
 
     def __init__(self, max_batch: int, max_pages_per_row: int, num_pages: int, hq: int = 32, hkv: int = 8,
-                 d: int = 128, split=(16, 64), target_tasks: int = 256, policy: int = 1, mlp: bool = False,
+                 d: int = 128, split=(16, 64), target_tasks: int = 0, policy: int = 1, mlp: bool = False,
                  mlp_width: int = 11008, seed: int = 0, device="cuda"):
         import torch
         self.torch = torch
@@ -96,7 +97,9 @@ class Engine:
         self.q = torch.zeros((max_batch, hq, d), dtype=torch.float16, device=self.dev)
         self.out = torch.zeros((max_batch, hq, d), dtype=torch.float16, device=self.dev)
         self.bufs = _b.DecodeBuffers(max_batch, hq, hkv, d, split[1], self.dev)
-        self.params = _b.make_params(hkv, split[0], split[1], target_tasks, policy=policy)
+        # target 0: the cost model's rule, per step, from the active rows
+        self.split, self.policy, self.fixed_target = split, policy, target_tasks
+        self.params = _b.make_params(hkv, split[0], split[1], target_tasks or costmodel.CUS, policy=policy)
         self.mlp = None
         if mlp:
             h = hq * d
@@ -134,6 +137,8 @@ class Engine:
             self.q.normal_(generator=self.gen)
             self.q.mul_(1.0 / np.sqrt(self.d))
         self.lens.copy_(torch.from_numpy(self.lens_host))
+        if not self.fixed_target:
+            self.params.target_tasks = costmodel.default_target(idx.size, self.hkv)
         b = self.bufs
         _b.pkv_plan_decode(self.q, self.k, self.v, self.bt, self.lens, self.params, b.tasks, b.split_offsets,
                            b.num_tasks, 1.0, self.out, b.ws)
@@ -244,7 +249,7 @@ def main(argv=None) -> int:
     ap.add_argument("--decode", default="64,256", help="decode length range min,max")
     ap.add_argument("--arrival-gap", type=int, default=0)
     ap.add_argument("--mlp", action="store_true", help="gated-MLP tail (width 11008) after attention")
-    ap.add_argument("--target-tasks", type=int, default=256)
+    ap.add_argument("--target-tasks", type=int, default=0, help="0: the cost model's rule per step")
     ap.add_argument("--seed", type=int, default=20260623)
     args = ap.parse_args(argv)
     import torch

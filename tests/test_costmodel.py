@@ -84,3 +84,21 @@ def test_committed_calibration_loads():
     best, _ = cm.choose_route([32769], params(target=256, policy=1), cal,
                               routes=("one-launch", "plan+fused", "two-kernel", "rect"))
     assert best == "one-launch"
+
+
+def test_default_target_rule():
+    """One task per compute unit unless the KV heads need room for 4 splits per active
+    row (the measured optimum of every G and trace in the split sweep)."""
+    assert cm.default_target(1, 8) == 256            # B1, G = 4
+    assert cm.default_target(8, 8) == 256            # B8, G = 4
+    assert cm.default_target(8, 4) == 256            # B8, G = 8
+    assert cm.default_target(8, 16) == 512           # B8, G = 2
+    assert cm.default_target(8, 32) == 1024          # B8, G = 1
+    assert cm.default_target(4, 32) == 512           # B4, G = 1
+    assert cm.default_target(1, 32) == 256           # B1, G = 1
+    assert cm.default_target(0, 8) == 256            # an idle step still gets a valid target
+    # the planner never exceeds the task buffer whatever the target: B * Hkv * split_max
+    lens = [20000, 300, 0, 9000]
+    p = params(target=cm.default_target(3, 32), smin=1, smax=64, policy=1, hkv=32)
+    _, _, n = pkv.pkv_plan_host(lens, p, 2000, with_tasks=False)
+    assert n <= p.target_tasks and n <= len(lens) * 32 * 64
