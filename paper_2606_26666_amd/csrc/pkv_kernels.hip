@@ -7,15 +7,14 @@
 //   merge_kernel    exact segmented merge of split states (Sec. 3.3)
 //
 // Work mapping. One workgroup owns one task: one KV head g of one row and a token
-// range [t0, t1). Its W wavefronts take the range's 16-token pages round-robin. A
-// wavefront reads one page of one head as four 1 KiB loads: lane (r, c) = (lane/16,
-// lane%16) loads 16 bytes (8 halves, dims 8c..8c+7) of token 4i+r, so every load covers
-// four whole 256-byte head rows. Each lane keeps the G query vectors' matching 8 dims,
-// forms partial dot products with v_dot2_f32_f16 and a 16-lane DPP butterfly completes
-// them, so all 16 lanes of a row hold the scores of their token for all G query heads.
-// Each of the four lane rows then runs its own online softmax (m, l, acc[G][8 dims]) in
-// fp32 over the tokens it saw. At the end of the task a lane butterfly combines the
-// four rows of each wavefront and LDS combines the W wavefront states, in a fixed order.
+// range [t0, t1). Its W wavefronts take the range's 16-token pages round-robin, two
+// pages in flight per wave. Two task bodies: MfmaTask (G = 4, 8) forms Q.K^T and P.V on
+// the matrix cores; ValuTask (G = 1, 2) reads one page of one head as four 1 KiB loads
+// (lane (r, c) = (lane/16, lane%16) loads 16 bytes, dims 8c..8c+7, of token 4i+r, so
+// every load covers four whole 256-byte head rows), forms partial dot products with
+// v_dot2_f32_f16 completed by a 16-lane DPP butterfly, and runs an online softmax per
+// lane row (m, l, acc[G][8 dims]) in fp32. Each ends with an LDS combine of the W wave
+// states in a fixed order.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
