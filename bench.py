@@ -397,6 +397,18 @@ def cpu_baseline(runner, steps, budget_s=15.0):
             "tiny_step_ms": dt_tiny * 1e3}
 
 
+def oracle_step_tok_s(runner):
+    """The oracle's rate on one step of another workload (its first step's inputs, after
+    an untimed first-touch call), BLAS pool at its default size."""
+    from oracle import ref_decode
+    w = runner.w
+    k, v, q = runner.k.cpu().numpy(), runner.v.cpu().numpy(), runner.q.cpu().numpy()
+    ref_decode(q, k, v, w.block_table, w.lengths_at(0))
+    t0 = time.perf_counter()
+    ref_decode(q, k, v, w.block_table, w.lengths_at(0))
+    return w.batch / (time.perf_counter() - t0)
+
+
 CALIBRATION = os.path.join(ROOT, "paper_2606_26666_amd", "calibration_mi355x.json")
 # (workload, route, policy, task target) steps the cost model is fitted on: the split
 # sensitivity sweep of the one-launch workqueue plus every other route on the ragged
@@ -514,9 +526,12 @@ def main():
     s = summarize(main_run, m)
     extra = {args.workload: s, "calibration": cal,
              "cost_model": cost_model_view(main_run, s["ms_per_step"] * 1e3)}
+    oracle_also = {}
     for name in [x for x in args.also.split(",") if x and x != "none" and x != args.workload]:
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy, hkv=args.hkv)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
+        if name == "b8_bimodal" and not args.no_cpu_baseline:
+            oracle_also[name] = oracle_step_tok_s(r)
         del r
     for wl in [x for x in args.routes_table.split(",") if x and x != "none"]:
         table = {}
@@ -551,7 +566,9 @@ def main():
                      "kernel": "split_kernel" + (" (planner inside)" if args.route == "one-launch" else ""),
                      "alg_bytes_per_launch": s["alg_bytes_last_step"],
                      "kernel_source_sha256": kernel_hash()},
-        "cpu_baseline": None if args.no_cpu_baseline else cpu_baseline(main_run, args.steps),
+        "cpu_baseline": None if args.no_cpu_baseline else {
+            **cpu_baseline(main_run, args.steps),
+            **{f"{k}_step_tok_s": val for k, val in oracle_also.items()}},
         "extra": extra,
     }
     print(json.dumps(line))

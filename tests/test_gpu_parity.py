@@ -289,7 +289,7 @@ def test_plan_decode_repeated_and_changing_lengths():
     assert pkv.pkv_check_device_status(bufs.ws) == 0
 
 
-@pytest.mark.parametrize("name", ["b1", "b8_bimodal"])
+@pytest.mark.parametrize("name", ["b1", "b8_bimodal", "b8_uniform", "b8_zipf", "b4_bimodal"])
 def test_plan_decode_benchmark_configs(name):
     case, w = Case.from_workload(name)
     p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens)
@@ -300,16 +300,23 @@ def test_plan_decode_benchmark_configs(name):
     assert np.array_equal(tasks, oracle_plan(case, p)[0])
 
 
-@pytest.mark.parametrize("name,hkv", [("b1", 32), ("b1", 4), ("b8_bimodal", 32), ("b8_bimodal", 4)])
+@pytest.mark.parametrize("name,hkv", [("b1", 32), ("b1", 4), ("b8_bimodal", 32), ("b8_bimodal", 4),
+                                      ("b8_uniform", 16), ("b4_bimodal", 32)])
 def test_plan_decode_gqa_mappings_full_size(name, hkv):
-    """G = 1 (32 KV heads) and G = 8 (4 KV heads) on the benchmark lengths, one launch."""
+    """G = 1, 2 and 8 on the benchmark lengths, one launch, with the task target the
+    bench uses (the cost model's rule: 1024 tasks for B8 at 32 KV heads, so workgroups
+    loop over several tasks after their speculative first one)."""
+    from paper_2606_26666_amd import costmodel
     case, w = Case.from_workload(name, hkv=hkv)
-    p = plan_params(w.hkv, w.split_min, w.split_max, w.target_tasks, w.tile_tokens, policy=1)
+    target = costmodel.default_target(int(np.count_nonzero(case.lens)), w.hkv)
+    p = plan_params(w.hkv, w.split_min, w.split_max, target, w.tile_tokens, policy=1)
     bufs = bufs_for(case, w.split_max)
     out = run_plan_decode(case, bufs, p)
     assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"{name} G={32 // hkv}")
     tasks, _ = read_plan(bufs)
     assert np.array_equal(tasks, oracle_plan(case, p)[0])
+    again = run_plan_decode(case, bufs, p)  # every first task now starts from its hint
+    assert torch.equal(again, out)
     assert pkv.pkv_check_device_status(bufs.ws) == 0
 
 
