@@ -206,7 +206,9 @@ def pkv_plan_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tenso
                     seq_lens: torch.Tensor, params: PlanParams, tasks: torch.Tensor, split_offsets: torch.Tensor,
                     num_tasks: torch.Tensor, sm_scale: float, out: torch.Tensor, ws: torch.Tensor, *, stream=None,
                     events=None):
-    """events: optional (start, stop) timing events (pkv_plan_decode_timed)."""
+    """Plan, attend and merge in one launch (see include/pkv.h). `tasks` is written with the
+    plan; its previous contents are only a scheduling hint (any contents are allowed).
+    events: optional (start, stop) timing events (pkv_plan_decode_timed)."""
     B, Hq, d = q.shape
     num_pages, _, Hkv, _ = k_cache.shape
     ev = _events(events)
