@@ -24,7 +24,8 @@
  *    (a page id outside the pool, a length beyond the block table) set bits in the
  *    workspace's error word, read back by pkv_check_device_status, and the affected
  *    rows' outputs are written as zeros.
- *  - Concurrent calls on different streams need separate workspaces.
+ *  - Concurrent calls on different streams need separate workspaces and separate
+ *    output buffers (task list, split_offsets, num_tasks, out).
  */
 #ifndef PKV_H
 #define PKV_H

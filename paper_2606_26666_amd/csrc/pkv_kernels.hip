@@ -1223,14 +1223,13 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   if (PLAN) {
     if (wave_plan(a.plan)) {
       // Speculative start. Between decode steps a plan rarely changes (lengths grow by a
-      // token), so while the planner runs, each wave begins and primes the task listed
-      // at this workgroup's index in the task list left by the previous launch (the task
-      // it ran then): a hint, read with agent-scope loads because workgroup 0 rewrites
-      // the list meanwhile. A record
-      // is used only if it names a task inside the batch's bounds (the buffer may hold
-      // anything on the first call), and the begun loads are kept only if the new plan
-      // gives this workgroup a task they cover; otherwise the task is begun again. The
-      // results never depend on the hint.
+      // token), so while wave 0 runs the planner, each wave begins and primes the task
+      // listed at this workgroup's index in the task list left by the previous launch
+      // (the task it ran then): a hint, read with agent-scope loads because workgroup 0
+      // rewrites the list meanwhile. A record is used only if it names a task inside the
+      // batch's bounds (the buffer may hold anything on the first call), and the begun
+      // loads are kept only if the new plan gives this workgroup a task they cover;
+      // otherwise the task is begun again. The results never depend on the hint.
       const int n_raw = threadIdx.x < 64 ? wave_plan_len(a.plan) : 0;  // the planner's load goes first
       if ((int)blockIdx.x < a.max_tasks) {
         const int* tp = reinterpret_cast<const int*>(a.tasks + blockIdx.x);
