@@ -87,7 +87,7 @@ class Runner:
         w = make_workload(name, seed=seed, steps=steps, hkv=hkv)
         if not target_tasks:  # the cost model's rule for the first step's active rows
             from paper_2606_26666_amd import costmodel
-            target_tasks = costmodel.default_target(int(np.count_nonzero(w.lengths_at(0))), w.hkv)
+            target_tasks = costmodel.default_target(int(np.count_nonzero(w.lengths_at(0))), w.hkv, hq=w.hq)
         self.w = w = dataclasses.replace(w, target_tasks=target_tasks)
         self.dev = torch.device("cuda:0")
         shape = (w.num_pages, w.page_size, w.hkv, w.head_dim)
@@ -462,6 +462,28 @@ def cost_model_view(runner, measured_us):
                             "launch_us": cal.launch_us, "c_min": cal.c_min, "fixed_us": cal.fixed_us}}
 
 
+def seed_spread(args, workloads, seeds, first, flush_bufs):
+    """Per-seed tok/s, step time and decode-kernel bandwidth of each workload on the main
+    seed (results already in `first`) and the further held-out seeds, with mean and
+    sample std over all of them (the paper reports mean and std over five held-out
+    seeds)."""
+    keys = ("tok_s", "ms_per_step", "decode_ms", "decode_gbs")
+    out = {}
+    for name in workloads:
+        per = {str(args.seed): {k: first[name][k] for k in keys}}
+        for sd in seeds:
+            steps = 20 if name == "b1" else 50
+            r = Runner(name, sd, args.target_tasks, steps, route=args.route, policy=args.policy, hkv=args.hkv)
+            res = summarize(r, measure(r, min(args.steps * 2, steps), args.warmup, flush_bufs))
+            per[str(sd)] = {k: res[k] for k in keys}
+            del r
+        out[name] = {"per_seed": per,
+                     **{k + "_mean": float(np.mean([v[k] for v in per.values()])) for k in keys},
+                     **{k + "_std": float(np.std([v[k] for v in per.values()], ddof=1)) if len(per) > 1 else 0.0
+                        for k in keys}}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -470,6 +492,9 @@ def main():
     ap.add_argument("--workload", default="b1")
     ap.add_argument("--also", default="b8_bimodal", help="comma-separated extra workloads, or 'none'")
     ap.add_argument("--seed", type=int, default=20260623)
+    ap.add_argument("--seeds", default="20260624,20260625,20260626,20260627",
+                    help="further held-out seeds: the main workload and each --also workload are also run "
+                         "on these, and extra.seeds reports mean and std over --seed plus these ('none' to skip)")
     ap.add_argument("--target-tasks", type=int, default=0,
                     help="planner task target; 0 = the cost model's rule, max(256, 4 * Hkv * active rows) "
                          "(256 = one task per compute unit)")
@@ -527,12 +552,17 @@ def main():
     extra = {args.workload: s, "calibration": cal,
              "cost_model": cost_model_view(main_run, s["ms_per_step"] * 1e3)}
     oracle_also = {}
-    for name in [x for x in args.also.split(",") if x and x != "none" and x != args.workload]:
+    also = [x for x in args.also.split(",") if x and x != "none" and x != args.workload]
+    for name in also:
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy, hkv=args.hkv)
         extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
         if name == "b8_bimodal" and not args.no_cpu_baseline:
             oracle_also[name] = oracle_step_tok_s(r)
         del r
+    seeds = [int(x) for x in args.seeds.split(",") if x and x != "none" and int(x) != args.seed]
+    if seeds:
+        extra["seeds"] = seed_spread(args, [args.workload] + also, seeds,
+                                     {args.workload: s, **{n: extra[n] for n in also}}, flush_bufs)
     for wl in [x for x in args.routes_table.split(",") if x and x != "none"]:
         table = {}
         for route in ROUTES:

@@ -14,7 +14,9 @@
 // every load covers four whole 256-byte head rows), forms partial dot products with
 // v_dot2_f32_f16 completed by a 16-lane DPP butterfly, and runs an online softmax per
 // lane row (m, l, acc[G][8 dims]) in fp32. Each ends with an LDS combine of the W wave
-// states in a fixed order.
+// states in a fixed order. The one-launch route can give a workgroup KV heads g and
+// g + 1 of one split instead (MfmaTask with NH = 2, one page in flight per head), which
+// balances the per-head read rates across workgroups.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -143,43 +145,50 @@ constexpr int kRunsPerBlock = kMergeBlock / kMergeRun;
 constexpr int kMaxMergeWaves = 16;
 constexpr int kOutOfRange = (int)0x80000000u;  // buffer offset past any slot buffer
 
-template <int G>
+template <int G, int NH = 1>
 constexpr int merge_lds_floats() {
-  return 2 * kMergeBlock * G + kRunsPerBlock * G * D + kRunsPerBlock * G + 2 * kMaxMergeWaves * G + 3 * G;
+  constexpr int GH = NH * G;
+  return 2 * kMergeBlock * GH + kRunsPerBlock * GH * D + kRunsPerBlock * GH + 2 * kMaxMergeWaves * GH + 3 * GH;
 }
 
 // The nsplit states at slots slot0 + s*stride (s < nsplit) of one (row, KV head) into
-// out_grp[G][D] (fp16). All NT threads of the workgroup take part.
-template <int G, int NT, bool COHERENT>
+// out_grp[G][D] (fp16). All NT threads of the workgroup take part. NH = 2 merges KV
+// heads g and g + 1 of the row together (their slots are adjacent: slot0 + s*stride + 1
+// is head g + 1's) into out_grp[2G][D]; every output element goes through the same
+// operations, in the same order, as in a one-head merge.
+template <int G, int NT, bool COHERENT, int NH = 1>
 __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0, int stride, int nsplit,
                                             uint16_t* __restrict__ out_grp, float* lds) {
-  static_assert(NT % 64 == 0 && NT / 64 <= kMaxMergeWaves && 64 % G == 0, "merge shape");
-  constexpr int SB = slot_floats<G>() * 4;            // slot bytes
-  constexpr int E4 = G * D / 4;                       // float4 columns of the output
-  constexpr int EPT = (G * D + NT - 1) / NT;          // output elements per thread
-  constexpr int KPT = (kMergeBlock * G + NT - 1) / NT;  // (split, head) states per thread
-  float* lw = lds;                                    // [block][G] weights 2^(m-M)
-  float* ll = lw + kMergeBlock * G;                   // [block][G] l
-  float* part = ll + kMergeBlock * G;                 // [run][G*D] run sums of acc
-  float* partL = part + kRunsPerBlock * G * D;        // [run][G] run sums of l
-  float* redM = partL + kRunsPerBlock * G;            // [wave][G]
-  float* redB = redM + kMaxMergeWaves * G;            // [wave][G]
-  float* sM = redB + kMaxMergeWaves * G;              // [G] max
-  float* sBad = sM + G;                               // [G]
-  float* sL = sBad + G;                               // [G] running L
+  constexpr int GH = NH * G;                           // query heads merged
+  static_assert(NT % 64 == 0 && NT / 64 <= kMaxMergeWaves && 64 % GH == 0, "merge shape");
+  constexpr int SB = slot_floats<G>() * 4;             // slot bytes
+  constexpr int E4H = G * D / 4;                       // float4 columns per KV head
+  constexpr int E4 = NH * E4H;                         // float4 columns of the output
+  constexpr int EPT = (GH * D + NT - 1) / NT;          // output elements per thread
+  constexpr int KPT = (kMergeBlock * GH + NT - 1) / NT;  // (split, head) states per thread
+  float* lw = lds;                                     // [block][GH] weights 2^(m-M)
+  float* ll = lw + kMergeBlock * GH;                   // [block][GH] l
+  float* part = ll + kMergeBlock * GH;                 // [run][GH*D] run sums of acc
+  float* partL = part + kRunsPerBlock * GH * D;        // [run][GH] run sums of l
+  float* redM = partL + kRunsPerBlock * GH;            // [wave][GH]
+  float* redB = redM + kMaxMergeWaves * GH;            // [wave][GH]
+  float* sM = redB + kMaxMergeWaves * GH;              // [GH] max
+  float* sBad = sM + GH;                               // [GH]
+  float* sL = sBad + GH;                               // [GH] running L
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int myh = tid % G;  // the head of every (split, head) state this thread loads
-  auto soff = [&](int s) { return (slot0 + s * stride) * SB; };
+  const int myh = tid % GH;  // the head of every (split, head) state this thread loads
+  const int my_hh = myh / G, my_h = myh % G;
+  auto soff = [&](int s, int hh) { return (slot0 + s * stride + hh) * SB; };
 
   float mv[KPT], lv[KPT];
   auto load_ml = [&](int s0, int cnt) {
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
       const int e = tid + k * NT;
-      const bool ok = e < cnt * G;
-      const int off = ok ? soff(s0 + e / G) + (G * D + myh) * 4 : kOutOfRange;
+      const bool ok = e < cnt * GH;
+      const int off = ok ? soff(s0 + e / GH, my_hh) + (G * D + my_h) * 4 : kOutOfRange;
       const float m = ld_state<COHERENT>(pr, off);
       lv[k] = ld_state<COHERENT>(pr, off + G * 4);  // l sits G floats after m (0 when absent)
       mv[k] = ok ? m : kNegInf;
@@ -195,20 +204,20 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
       bd = fmaxf(bd, lv[k] < 0.0f ? 1.0f : 0.0f);
     }
 #pragma unroll
-    for (int sh = G; sh < 64; sh <<= 1) {
+    for (int sh = GH; sh < 64; sh <<= 1) {
       mx = fmaxf(mx, __shfl_xor(mx, sh));
       bd = fmaxf(bd, __shfl_xor(bd, sh));
     }
-    if (lane < G) {
-      redM[wave * G + lane] = mx;
-      redB[wave * G + lane] = bd;
+    if (lane < GH) {
+      redM[wave * GH + lane] = mx;
+      redB[wave * GH + lane] = bd;
     }
     __syncthreads();
-    if (tid < G) {
+    if (tid < GH) {
       float m2 = sM[tid], b2 = sBad[tid];
       for (int w = 0; w < NT / 64; ++w) {
-        m2 = fmaxf(m2, redM[w * G + tid]);
-        b2 = fmaxf(b2, redB[w * G + tid]);
+        m2 = fmaxf(m2, redM[w * GH + tid]);
+        b2 = fmaxf(b2, redB[w * GH + tid]);
       }
       sM[tid] = m2;
       sBad[tid] = b2;
@@ -216,7 +225,7 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     __syncthreads();
   };
 
-  if (tid < G) {
+  if (tid < GH) {
     sM[tid] = kNegInf;
     sBad[tid] = 0.0f;
     sL[tid] = 0.0f;
@@ -238,17 +247,18 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     const int nitems = E4 * nrun;
     auto issue_item = [&](int it) {  // it >= nitems: every load is out of range (zeros)
       const int e4 = it % E4;
+      const int hh = e4 / E4H;
       const int sb = (it / E4) * kMergeRun;
       const int n = min(kMergeRun, cnt - sb);
 #pragma unroll
       for (int u = 0; u < kMergeRun; ++u)
-        v[u] = ld_state4<COHERENT>(pr, u < n ? soff(s0 + sb + u) + e4 * 16 : kOutOfRange);
+        v[u] = ld_state4<COHERENT>(pr, u < n ? soff(s0 + sb + u, hh) + (e4 - hh * E4H) * 16 : kOutOfRange);
     };
     auto finish_item = [&](int it) {
-      const int e4 = it % E4;
+      const int e4 = it % E4;  // = hh * E4H + column within KV head hh
       const int run = it / E4;
       const int sb = run * kMergeRun;
-      const int h = (e4 * 4) / D;
+      const int h = (e4 * 4) / D;  // query head within the GH merged
       v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
       float lacc = 0.0f;
       const bool first_col = (e4 * 4) % D == 0;
@@ -256,15 +266,15 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
       // sum that starts at +0 leaves it unchanged, so no per-split branch is needed
 #pragma unroll
       for (int u = 0; u < kMergeRun; ++u) {
-        const float w = lw[(sb + u) * G + h];
+        const float w = lw[(sb + u) * GH + h];
         acc.x = __builtin_fmaf(w, v[u].x, acc.x);
         acc.y = __builtin_fmaf(w, v[u].y, acc.y);
         acc.z = __builtin_fmaf(w, v[u].z, acc.z);
         acc.w = __builtin_fmaf(w, v[u].w, acc.w);
-        lacc = __builtin_fmaf(w, ll[(sb + u) * G + h], lacc);
+        lacc = __builtin_fmaf(w, ll[(sb + u) * GH + h], lacc);
       }
-      *reinterpret_cast<v4f*>(part + run * G * D + e4 * 4) = acc;
-      if (first_col) partL[run * G + h] = lacc;
+      *reinterpret_cast<v4f*>(part + run * GH * D + e4 * 4) = acc;
+      if (first_col) partL[run * GH + h] = lacc;
     };
     __syncthreads();  // the previous block's LDS is consumed
     load_ml(s0, cnt);
@@ -273,9 +283,9 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
       const int e = tid + k * NT;
-      if (e < kMergeBlock * G) {
+      if (e < kMergeBlock * GH) {
         const float M = sM[myh];
-        const bool ok = e < cnt * G;
+        const bool ok = e < cnt * GH;
         lw[e] = ok ? ex2(mv[k] - (M == kNegInf ? 0.0f : M)) : 0.0f;
         ll[e] = ok ? lv[k] : 0.0f;
       }
@@ -290,17 +300,17 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
 #pragma unroll
     for (int q = 0; q < EPT; ++q) {
       const int e = tid + q * NT;
-      if (e < G * D)
-        for (int run = 0; run < nrun; ++run) A[q] += part[run * G * D + e];
+      if (e < GH * D)
+        for (int run = 0; run < nrun; ++run) A[q] += part[run * GH * D + e];
     }
-    if (tid < G)
-      for (int run = 0; run < nrun; ++run) sL[tid] += partL[run * G + tid];
+    if (tid < GH)
+      for (int run = 0; run < nrun; ++run) sL[tid] += partL[run * GH + tid];
   }
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < EPT; ++q) {
     const int e = tid + q * NT;
-    if (e >= G * D) break;
+    if (e >= GH * D) break;
     const int h = e / D;
     const float o = (sM[h] == kNegInf || sBad[h] != 0.0f) ? 0.0f : A[q] / sL[h];
     out_grp[e] = f32_to_f16_bits(o);
@@ -311,12 +321,14 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
 // One task: KV head g of `row`, tokens [t0, t1), partial state into `slot`.
 // The task's partial state from the W wave states staged in LDS (m, l, acc per wave
 // and head, page-error flag per wave): a fixed-order combine, stored to slot `slot`.
-template <int G, int W, bool COHERENT>
+// NH = 2: the states of KV heads g and g + 1 (tasks `slot` and `slot` + 1), side by side
+// in LDS, each combined exactly as a one-head task's.
+template <int G, int W, bool COHERENT, int NH = 1>
 __device__ __forceinline__ void finish_task(const DecodeArgs& a, int slot, float* lds) {
-  float* lds_m = lds;                // [W][G]
-  float* lds_l = lds + W * G;        // [W][G]
-  float* lds_acc = lds + 2 * W * G;  // [W][G][D]
-  int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
+  float* lds_m = lds;                     // [NH][W][G]
+  float* lds_l = lds + NH * W * G;        // [NH][W][G]
+  float* lds_acc = lds + 2 * NH * W * G;  // [NH][W][G][D]
+  int* lds_bad = reinterpret_cast<int*>(lds + 2 * NH * W * G + NH * W * G * D);
 
   bool any_bad = false;
 #pragma unroll
@@ -324,29 +336,36 @@ __device__ __forceinline__ void finish_task(const DecodeArgs& a, int slot, float
   if (any_bad && threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_PAGE_ID);
 
   constexpr int SB = slot_floats<G>() * 4;
+  constexpr int E4H = G * D / 4;  // float4 columns per head
   const __amdgpu_buffer_rsrc_t pr = slots_rsrc(a, SB);
-  for (int e4 = threadIdx.x; e4 < G * D / 4; e4 += W * 64) {
+  for (int e4g = threadIdx.x; e4g < NH * E4H; e4g += W * 64) {
+    const int hh = e4g / E4H;
+    const int e4 = e4g - hh * E4H;
     const int h = (e4 * 4) / D;
+    const float* hm = lds_m + hh * W * G;
+    const float* hl = lds_l + hh * W * G;
+    const float* hacc = lds_acc + (size_t)hh * W * G * D;
+    const int so = (slot + hh) * SB;
     float M = kNegInf;
 #pragma unroll
-    for (int w = 0; w < W; ++w) M = fmaxf(M, lds_m[w * G + h]);
+    for (int w = 0; w < W; ++w) M = fmaxf(M, hm[w * G + h]);
     const float Mref = (M == kNegInf) ? 0.0f : M;
     float L = 0.0f;
     v4f A = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int w = 0; w < W; ++w) {
-      const float cf = ex2(lds_m[w * G + h] - Mref);
-      const v4f x = *reinterpret_cast<const v4f*>(lds_acc + (size_t)w * G * D + e4 * 4);
-      L = __builtin_fmaf(cf, lds_l[w * G + h], L);
+      const float cf = ex2(hm[w * G + h] - Mref);
+      const v4f x = *reinterpret_cast<const v4f*>(hacc + (size_t)w * G * D + e4 * 4);
+      L = __builtin_fmaf(cf, hl[w * G + h], L);
       A.x = __builtin_fmaf(cf, x.x, A.x);
       A.y = __builtin_fmaf(cf, x.y, A.y);
       A.z = __builtin_fmaf(cf, x.z, A.z);
       A.w = __builtin_fmaf(cf, x.w, A.w);
     }
-    st_state4<COHERENT>(pr, slot * SB + e4 * 16, A);
+    st_state4<COHERENT>(pr, so + e4 * 16, A);
     if ((e4 * 4) % D == 0) {
-      st_state<COHERENT>(pr, slot * SB + (G * D + h) * 4, M);
-      st_state<COHERENT>(pr, slot * SB + (G * D + G + h) * 4, any_bad ? -1.0f : L);
+      st_state<COHERENT>(pr, so + (G * D + h) * 4, M);
+      st_state<COHERENT>(pr, so + (G * D + G + h) * 4, any_bad ? -1.0f : L);
     }
   }
 }
@@ -590,13 +609,20 @@ constexpr bool mfma_task() {
   return G == 4 || G == 8;
 }
 
-// The phases and covers() are those of ValuTask.
-template <int G, int W>
+// The phases and covers() are those of ValuTask. NH = 2 runs KV heads g and g + 1 of
+// the same (row, split) together: each wave reads both heads of a page (adjacent
+// 256-byte slices of every token), one page ahead per head, and keeps one softmax state
+// per head. Each head's state goes through exactly the operations the one-head body
+// applies to it, in the same order, so its result is bitwise that of the one-head body.
+template <int G, int W, int NH = 1>
 struct MfmaTask {
   static_assert(G <= 16, "heads fit the 16 MFMA columns");
+  static_assert(NH == 1 || NH == 2, "one or two KV heads per task body");
   int row = 0, g = 0, t0 = 0, pg_end = 0, first = 0, npw = 0, ids = 0;  // npw = 0: no task begun
   bool bad = false;
-  v4u qb[4];
+  v4u qb[NH][4];
+  // NH = 1: pages j (ka, va) and j + 1 (kb, vb); NH = 2: page j of head g (ka, va) and of
+  // head g + 1 (kb, vb)
   v4u ka[4], va[4], kb[4], vb[4];
 
   __device__ __forceinline__ void begin(const DecodeArgs& a, int row_, int g_, int t0_, int t1_) {
@@ -612,11 +638,14 @@ struct MfmaTask {
     npw = uniform(first < pg_end ? (pg_end - first + W - 1) / W : 0);
     bad = false;
     const bool hv = col < G;
-    const uint16_t* qh = a.q + ((size_t)row * a.Hq + (size_t)g * G + (hv ? col : 0)) * D;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const v4u z = {0u, 0u, 0u, 0u};
-      qb[kb] = hv ? *reinterpret_cast<const v4u*>(qh + kb * 32 + 8 * grp) : z;
+    for (int hh = 0; hh < NH; ++hh) {
+      const uint16_t* qh = a.q + ((size_t)row * a.Hq + (size_t)(g + hh) * G + (hv ? col : 0)) * D;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        const v4u z = {0u, 0u, 0u, 0u};
+        qb[hh][kb] = hv ? *reinterpret_cast<const v4u*>(qh + kb * 32 + 8 * grp) : z;
+      }
     }
     ids = lane < npw ? a.block_table[(size_t)row * a.max_pages_per_row + first + lane * W] : 0;
   }
@@ -625,18 +654,20 @@ struct MfmaTask {
     return row_ == row && g_ == g && t0_ == t0 && (t1_ + P - 1) / P == pg_end;
   }
 
-  __device__ __forceinline__ void issue(const DecodeArgs& a, v4u (&kr)[4], v4u (&vr)[4], int j, bool live) {
-    issue_page(a, kr, vr, __builtin_amdgcn_readlane(ids, j), live);
+  __device__ __forceinline__ void issue(const DecodeArgs& a, v4u (&kr)[4], v4u (&vr)[4], int j, bool live,
+                                        int hh = 0) {
+    issue_page(a, kr, vr, __builtin_amdgcn_readlane(ids, j), live, hh);
   }
-  __device__ __forceinline__ void issue_page(const DecodeArgs& a, v4u (&kr)[4], v4u (&vr)[4], int phys, bool live) {
+  __device__ __forceinline__ void issue_page(const DecodeArgs& a, v4u (&kr)[4], v4u (&vr)[4], int phys, bool live,
+                                             int hh = 0) {
     const int lane = threadIdx.x & 63;
     const int grp = lane >> 4;
     const int col = lane & 15;
     const size_t tok_stride = (size_t)a.Hkv * D;  // halves between consecutive tokens
     const size_t page_stride = (size_t)P * tok_stride;
     const int tok_b = (int)(tok_stride * 2);
-    const int k_off = col * tok_b + g * D * 2 + grp * 16;  // + 64 kb
-    const int v_off = grp * tok_b + g * D * 2 + col * 16;  // + 4 i tok_b
+    const int k_off = col * tok_b + (g + hh) * D * 2 + grp * 16;  // + 64 kb
+    const int v_off = grp * tok_b + (g + hh) * D * 2 + col * 16;  // + 4 i tok_b
     const bool ok = phys >= 0 && phys < a.num_pages;
     bad |= live && !ok;
     const int page_bytes = uniform(live ? (int)(page_stride * 2) : 0);
@@ -653,36 +684,48 @@ struct MfmaTask {
   // path out of prime() has waited for the id load and issued the same loads, and the
   // page loop's wait counts stay exact.
   __device__ __forceinline__ void prime(const DecodeArgs& a) {
-    issue(a, ka, va, 0, npw > 0);
-    issue(a, kb, vb, 1, npw > 1);
+    if constexpr (NH == 1) {
+      issue(a, ka, va, 0, npw > 0);
+      issue(a, kb, vb, 1, npw > 1);
+    } else {
+      issue(a, ka, va, 0, npw > 0, 0);
+      issue(a, kb, vb, 0, npw > 0, 1);
+    }
   }
 
   template <bool COHERENT>
   __device__ __forceinline__ void run(const DecodeArgs& a, int t1, int slot, float* lds) {
     __shared__ v4u vstage[W][P * D / 8];  // one V page of one head per wave: 16 rows of 256 B
-    float* lds_m = lds;                // [W][G]
-    float* lds_l = lds + W * G;        // [W][G]
-    float* lds_acc = lds + 2 * W * G;  // [W][G][D]
-    int* lds_bad = reinterpret_cast<int*>(lds + 2 * W * G + W * G * D);
+    float* lds_m = lds;                     // [NH][W][G]
+    float* lds_l = lds + NH * W * G;        // [NH][W][G]
+    float* lds_acc = lds + 2 * NH * W * G;  // [NH][W][G][D]
+    int* lds_bad = reinterpret_cast<int*>(lds + 2 * NH * W * G + NH * W * G * D);
     const int lane = threadIdx.x & 63;
     const int wave = uniform(threadIdx.x >> 6);
     const int grp = lane >> 4;
     const int col = lane & 15;
 
-    float m = kNegInf, l = 0.0f;
-    v4f acc[D / 16];
+    float m[NH], l[NH];
+    v4f acc[NH][D / 16];
 #pragma unroll
-    for (int db = 0; db < D / 16; ++db) acc[db] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int hh = 0; hh < NH; ++hh) {
+      m[hh] = kNegInf;
+      l[hh] = 0.0f;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) acc[hh][db] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+    }
     v4u* vst = &vstage[wave][0];
     const int tr_off = (4 * grp + (col >> 2)) * (D * 2) + (col & 3) * 8;  // + 32 db
 
-    auto consume = [&](v4u (&kr)[4], v4u (&vr)[4], int k) {
+    // one page of one head into that head's state (m, l, acc) with its query block qh
+    auto consume = [&](v4u (&kr)[4], v4u (&vr)[4], int k, float& m, float& l, v4f (&acc)[D / 16],
+                       const v4u (&qh)[4]) {
       const int pg = first + k * W;
       const bool tail = pg * P + P > t1;  // the row's last, partial page
       v4f sc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[kb]), __builtin_bit_cast(h8v, qb[kb]),
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[kb]), __builtin_bit_cast(h8v, qh[kb]),
                                                     sc, 0, 0, 0);
       // stage V token-major; rows past t1 are zeroed (their p is 0, but 0 * NaN is not)
 #pragma unroll
@@ -731,52 +774,77 @@ struct MfmaTask {
 
     for (int k0 = 0; k0 < npw; k0 += 64) {
       const int n = min(64, npw - k0);
-      if (k0 > 0) {  // begin() and prime() did this for the first id block
-        ids = (k0 + lane < npw) ? a.block_table[(size_t)row * a.max_pages_per_row + first + (k0 + lane) * W] : 0;
-        issue(a, ka, va, 0, true);
-        issue(a, kb, vb, 1, n > 1);
+      if constexpr (NH == 1) {
+        if (k0 > 0) {  // begin() and prime() did this for the first id block
+          ids = (k0 + lane < npw) ? a.block_table[(size_t)row * a.max_pages_per_row + first + (k0 + lane) * W] : 0;
+          issue(a, ka, va, 0, true);
+          issue(a, kb, vb, 1, n > 1);
+        }
+        // pages j (ka) and j + 1 (kb) are in flight at the top of each iteration
+        int j = 0;
+        for (; j + 2 < n; j += 2) {
+          consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
+          issue(a, ka, va, j + 2, true);
+          consume(kb, vb, k0 + j + 1, m[0], l[0], acc[0], qb[0]);
+          issue(a, kb, vb, (j + 3) & 63, j + 3 < n);
+        }
+        consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
+        if (j + 1 < n) consume(kb, vb, k0 + j + 1, m[0], l[0], acc[0], qb[0]);
+      } else {
+        if (k0 > 0) {
+          ids = (k0 + lane < npw) ? a.block_table[(size_t)row * a.max_pages_per_row + first + (k0 + lane) * W] : 0;
+          issue(a, ka, va, 0, true, 0);
+          issue(a, kb, vb, 0, true, 1);
+        }
+        // page j of both heads is in flight at the top of each iteration
+        int j = 0;
+        for (; j + 1 < n; ++j) {
+          consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
+          issue(a, ka, va, j + 1, true, 0);
+          consume(kb, vb, k0 + j, m[NH - 1], l[NH - 1], acc[NH - 1], qb[NH - 1]);
+          issue(a, kb, vb, j + 1, true, 1);
+        }
+        consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
+        consume(kb, vb, k0 + j, m[NH - 1], l[NH - 1], acc[NH - 1], qb[NH - 1]);
       }
-      // pages j (ka) and j + 1 (kb) are in flight at the top of each iteration
-      int j = 0;
-      for (; j + 2 < n; j += 2) {
-        consume(ka, va, k0 + j);
-        issue(a, ka, va, j + 2, true);
-        consume(kb, vb, k0 + j + 1);
-        issue(a, kb, vb, (j + 3) & 63, j + 3 < n);
-      }
-      consume(ka, va, k0 + j);
-      if (j + 1 < n) consume(kb, vb, k0 + j + 1);
     }
 
-    // wave state: m per head (shared by the groups), l summed over the groups, acc
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    if (col < G) {
+    // wave state per head: m per head (shared by the groups), l summed over the groups, acc
 #pragma unroll
-      for (int db = 0; db < D / 16; ++db)
-        *reinterpret_cast<v4f*>(lds_acc + ((size_t)wave * G + col) * D + 16 * db + 4 * grp) = acc[db];
-      if (grp == 0) {
-        lds_m[wave * G + col] = m;
-        lds_l[wave * G + col] = l;
+    for (int hh = 0; hh < NH; ++hh) {
+      float lw = l[hh];
+      lw += __shfl_xor(lw, 16);
+      lw += __shfl_xor(lw, 32);
+      if (col < G) {
+#pragma unroll
+        for (int db = 0; db < D / 16; ++db)
+          *reinterpret_cast<v4f*>(lds_acc + (((size_t)hh * W + wave) * G + col) * D + 16 * db + 4 * grp) =
+              acc[hh][db];
+        if (grp == 0) {
+          lds_m[(hh * W + wave) * G + col] = m[hh];
+          lds_l[(hh * W + wave) * G + col] = lw;
+        }
       }
     }
     if (lane == 0) lds_bad[wave] = bad ? 1 : 0;
     __syncthreads();
-    finish_task<G, W, COHERENT>(a, slot, lds);
+    finish_task<G, W, COHERENT, NH>(a, slot, lds);
   }
 };
 
-// The task body each route runs: matrix-core products for G = 4 and 8, VALU otherwise.
-template <bool MFMA, int G, int W>
+// The task body each route runs: matrix-core products for G = 4 and 8, VALU otherwise
+// (one KV head per body).
+template <bool MFMA, int G, int W, int NH>
 struct BodySel {
+  static_assert(NH == 1, "the VALU body runs one KV head");
   using type = ValuTask<G, W>;
 };
-template <int G, int W>
-struct BodySel<true, G, W> {
-  using type = MfmaTask<G, W>;
+template <int G, int W, int NH>
+struct BodySel<true, G, W, NH> {
+  using type = MfmaTask<G, W, NH>;
 };
-template <int G, int W>
-using TaskBody = typename BodySel<mfma_task<G>(), G, W>::type;
+template <int G, int W, int NH = 1>
+using TaskBody = typename BodySel<mfma_task<G>(), G, W, NH>::type;
 
 template <int G, int W, bool COHERENT>
 __device__ __forceinline__ void run_split_task(const DecodeArgs& a, int row, int g, int t0, int t1, int slot,
@@ -801,9 +869,9 @@ __device__ __forceinline__ void zero_row(const DecodeArgs& a, int row) {
   for (int e = threadIdx.x; e < a.Hq * D / 2; e += blockDim.x) o[e] = 0u;
 }
 
-template <int G, int W>
+template <int G, int W, int NH = 1>
 constexpr int lds_floats() {
-  return 2 * W * G + W * G * D + W;
+  return NH * (2 * W * G + W * G * D) + W;
 }
 
 // ---------------------------------------------------------------------------------
@@ -1198,11 +1266,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(PlanArgs a) {
 // Workqueue split kernel. FUSED: the last split of each (row, KV head) to finish merges
 // all of that pair's splits in split order (Sec. 3.4, atomic completion counter).
 // PLAN: the planner runs inside the launch (see below).
+// NH = 2 (with PLAN and FUSED): a workgroup runs tasks 2p and 2p + 1 together, which the
+// plan's order makes KV heads g and g + 1 (g even) of one (row, split); one completion
+// counter per (row, head pair) counts them as one, and its last arriver merges both
+// heads. Spreading every workgroup's reads over two heads' slices of each token
+// balances the workgroups: on MI355X one workgroup streaming a single head's slices
+// runs up to ~20% slower or faster than another, depending on the slices' offset.
 
-template <int G, int W, bool FUSED, bool PLAN>
+template <int G, int W, bool FUSED, bool PLAN, int NH = 1>
 __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
-  __shared__ float lds[lds_floats<G, W>()];
-  __shared__ float lds_merge[FUSED ? merge_lds_floats<G>() : 1];
+  static_assert(NH == 1 || (NH == 2 && FUSED && PLAN), "head pairs run on the one-launch route");
+  __shared__ float lds[lds_floats<G, W, NH>()];
+  __shared__ float lds_merge[FUSED ? merge_lds_floats<G, NH>() : 1];
   __shared__ int lds_last;
   __shared__ int p_len[PLAN ? kMaxFusedPlanBatch : 1];
   __shared__ int p_off[PLAN ? kMaxFusedPlanBatch + 1 : 1];
@@ -1217,7 +1292,7 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   // the start, so later scalar loads of them do not wait on memory (after the planner,
   // and at the end of the last task).
   asm volatile("" ::"s"(a.q), "s"(a.partials), "s"(gridDim.x));
-  TaskBody<G, W> body;
+  TaskBody<G, W, NH> body;
   bool begun = false;  // this wave's body holds a task begun before the plan
   int plan_ntasks = 0;
   if (PLAN) {
@@ -1231,11 +1306,12 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       // loads are kept only if the new plan gives this workgroup a task they cover;
       // otherwise the task is begun again. The results never depend on the hint.
       const int n_raw = threadIdx.x < 64 ? wave_plan_len(a.plan) : 0;  // the planner's load goes first
-      if ((int)blockIdx.x < a.max_tasks) {
-        const int* tp = reinterpret_cast<const int*>(a.tasks + blockIdx.x);
+      if (NH * (int)blockIdx.x < a.max_tasks) {
+        const int* tp = reinterpret_cast<const int*>(a.tasks + NH * blockIdx.x);
         const int hr = uniform(ld_i32<true>(tp + 0)), hg = uniform(ld_i32<true>(tp + 1));
         const int h0 = uniform(ld_i32<true>(tp + 3)), h1 = uniform(ld_i32<true>(tp + 4));
-        if (hr >= 0 && hr < a.B && hg >= 0 && hg < a.Hkv && h0 >= 0 && h1 > h0 && h1 <= a.max_pages_per_row * P) {
+        if (hr >= 0 && hr < a.B && hg >= 0 && hg % NH == 0 && hg + NH <= a.Hkv && h0 >= 0 && h1 > h0 &&
+            h1 <= a.max_pages_per_row * P) {
           body.begin(a, hr, hg, h0, h1);
           begun = true;
         }
@@ -1267,19 +1343,20 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       rec[3] = tp[4];
     }
   };
-  if (!PLAN || (int)blockIdx.x < plan_ntasks) fetch(blockIdx.x);  // PLAN: only real tasks
+  if (!PLAN || NH * (int)blockIdx.x < plan_ntasks) fetch(NH * blockIdx.x);  // PLAN: only real tasks
   int ntasks = PLAN ? plan_ntasks : uniform(*a.num_tasks);
   if (ntasks > a.max_tasks) ntasks = a.max_tasks;
-  for (int t = blockIdx.x; t < ntasks; t += gridDim.x) {
-    if (t != (int)blockIdx.x) fetch(t);
+  // NH = 2: the plan's task count is Hkv times its split count, and Hkv is even
+  for (int t = NH * blockIdx.x; t + NH <= ntasks; t += NH * gridDim.x) {
+    if (t != NH * (int)blockIdx.x) fetch(t);
     const int row = uniform(rec[0]), g = uniform(rec[1]);
     const int t0 = uniform(rec[2]), t1 = uniform(rec[3]);
-    if (row < 0 || row >= a.B || g < 0 || g >= a.Hkv || t0 < 0 || t1 <= t0 ||
+    if (row < 0 || row >= a.B || g < 0 || g % NH != 0 || g + NH > a.Hkv || t0 < 0 || t1 <= t0 ||
         t1 > a.max_pages_per_row * P) {  // not a task of a valid plan: flag and skip
       if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
       continue;
     }
-    if (!(begun && t == (int)blockIdx.x && body.covers(row, g, t0, t1))) {
+    if (!(begun && t == NH * (int)blockIdx.x && body.covers(row, g, t0, t1))) {
       body.begin(a, row, g, t0, t1);
       body.prime(a);
     }
@@ -1306,8 +1383,8 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       }
       __syncthreads();
       if (lds_last) {
-        merge_group<G, W * 64, true>(slots_rsrc(a, slot_floats<G>() * 4), off * a.Hkv + g, a.Hkv, nsplit,
-                               a.out + ((size_t)row * a.Hq + (size_t)g * G) * D, lds_merge);
+        merge_group<G, W * 64, true, NH>(slots_rsrc(a, slot_floats<G>() * 4), off * a.Hkv + g, a.Hkv, nsplit,
+                                         a.out + ((size_t)row * a.Hq + (size_t)g * G) * D, lds_merge);
         if (threadIdx.x == 0) a.counters[row * a.Hkv + g] = 0;
       }
     }
@@ -1436,6 +1513,15 @@ hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t 
     return launch(split_kernel<G, W, true, false>, grid < resident ? grid : resident, W * 64, s, start, stop, a);
   }
   if (mode == 3) {
+    // KV-head pairs when the task target gives every resident workgroup two tasks
+    if constexpr (mfma_task<G>()) {
+      static const int resident2 = resident_blocks((const void*)split_kernel<G, W, true, true, 2>, W * 64);
+      if (a.Hkv % 2 == 0 && a.plan.target_tasks >= 2 * resident2) {
+        const int pairs = grid / 2;
+        return launch(split_kernel<G, W, true, true, 2>, pairs < resident2 ? pairs : resident2, W * 64, s, start,
+                      stop, a);
+      }
+    }
     static const int resident = resident_blocks((const void*)split_kernel<G, W, true, true>, W * 64);
     return launch(split_kernel<G, W, true, true>, grid < resident ? grid : resident, W * 64, s, start, stop, a);
   }

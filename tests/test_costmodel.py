@@ -88,9 +88,15 @@ def test_committed_calibration_loads():
 
 def test_default_target_rule():
     """One task per compute unit unless the KV heads need room for 4 splits per active
-    row (the measured optimum of every G and trace in the split sweep)."""
+    row (the measured optimum of every G and trace in the split sweep), and two per
+    compute unit where KV-head pairs run with at most 8 splits per row and head."""
     assert cm.default_target(1, 8) == 256            # B1, G = 4
-    assert cm.default_target(8, 8) == 256            # B8, G = 4
+    assert cm.default_target(8, 8) == 512            # B8, G = 4: KV-head pairs, two tasks per CU
+    assert cm.default_target(4, 8) == 256            # B4, G = 4: pair merges would grow
+    assert cm.default_target(16, 4) == 512           # 16 rows, G = 8: pairs
+    assert cm.default_target(8, 8, hq=8) == 256      # G = 1 body runs one head
+    assert cm.head_pairs(32, 8) and cm.head_pairs(32, 4) and not cm.head_pairs(32, 16)
+    assert not cm.head_pairs(12, 3)                  # odd KV-head count
     assert cm.default_target(8, 4) == 256            # B8, G = 8
     assert cm.default_target(8, 16) == 512           # B8, G = 2
     assert cm.default_target(8, 32) == 1024          # B8, G = 1

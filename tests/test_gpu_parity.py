@@ -365,14 +365,15 @@ def _two_launch(case, p, split_max):
     return out, tasks, offs
 
 
-@pytest.mark.parametrize("policy", [0, 1])
-def test_plan_decode_hints_never_change_results(policy):
+@pytest.mark.parametrize("policy,target", [(0, 200), (1, 200), (0, 600), (1, 520)])
+def test_plan_decode_hints_never_change_results(policy, target):
     """The one-launch route starts each workgroup on the task that the previous call
     listed at the workgroup's index. Whatever the task buffer holds (garbage, plausible
     but wrong records, the right records at the wrong slots, the exact plan), outputs
-    and the task list are bitwise those of the route without that start."""
+    and the task list are bitwise those of the route without that start. Targets of 512
+    and more run KV-head pairs, whose hint is the record at twice the index."""
     case = Case([900, 0, 17, 4096, 33, 2500, 1, 700], seed=21)
-    p = plan_params(8, 2, 16, 200, policy=policy)
+    p = plan_params(8, 2, 16, target, policy=policy)
     expect, tasks_ref, offs_ref = _two_launch(case, p, 16)
     assert np.array_equal(tasks_ref, oracle_plan(case, p)[0])
     r = np.random.Generator(np.random.PCG64(5))
@@ -398,14 +399,16 @@ def test_plan_decode_hints_never_change_results(policy):
         assert pkv.pkv_check_device_status(bufs.ws) == 0, label
 
 
-def test_plan_decode_speculation_across_growing_steps():
+@pytest.mark.parametrize("target", [256, 512])
+def test_plan_decode_speculation_across_growing_steps(target):
     """Decode steps with every row one token longer than at the previous step (pages and
     tiles fill and new ones start), one workspace throughout: each step's output is bitwise
-    that of the two-launch route, and its task list is the oracle's."""
+    that of the two-launch route, and its task list is the oracle's (target 512: KV-head
+    pairs)."""
     base = np.array([1000, 15, 4063, 31, 300, 2047, 64, 9000], dtype=np.int32)
     steps = 40
     case = Case(base + steps, seed=22)
-    p = plan_params(8, 1, 64, 256, policy=1)
+    p = plan_params(8, 1, 64, target, policy=1)
     bufs = bufs_for(case, 64)
     for s in range(steps + 1):
         lens = base + s
@@ -438,4 +441,48 @@ def test_plan_decode_batch_above_one_wave():
         tasks, offs = read_plan(bufs)
         plan = oracle_plan(case, p)
         assert np.array_equal(tasks, plan[0]) and np.array_equal(offs, plan[1]), rep
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("name,hkv,policy", [("b1", 8, 1), ("b8_bimodal", 8, 1), ("b8_uniform", 8, 0),
+                                             ("b8_zipf", 8, 1), ("b4_bimodal", 8, 1), ("b1", 4, 1),
+                                             ("b8_bimodal", 4, 1)])
+def test_plan_decode_head_pairs_full_size(name, hkv, policy):
+    """Task target 512 on the benchmark lengths: the one-launch route runs KV heads g and
+    g + 1 of a split in one workgroup (G = 4 and G = 8). Each head's arithmetic is that of
+    a one-head task, so the output is bitwise the plan-kernel + fused-kernel route's at the
+    same plan, and within tolerance of the oracle; a repeated call (every workgroup
+    starting from its hint) is bitwise the same."""
+    case, w = Case.from_workload(name, hkv=hkv)
+    p = plan_params(w.hkv, w.split_min, w.split_max, 512, w.tile_tokens, policy=policy)
+    expect, tasks_ref, offs_ref = _two_launch(case, p, w.split_max)
+    bufs = bufs_for(case, w.split_max)
+    out = run_plan_decode(case, bufs, p)
+    tasks, offs = read_plan(bufs)
+    assert np.array_equal(tasks, oracle_plan(case, p)[0])
+    assert np.array_equal(tasks, tasks_ref) and np.array_equal(offs, offs_ref)
+    assert torch.equal(out, expect), name
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"{name} pairs G={32 // hkv}")
+    again = run_plan_decode(case, bufs, p)
+    assert torch.equal(again, out)
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("lens,target", [([1], 512), ([16, 0, 17], 512), ([0, 5000, 0, 5000, 4000], 4096),
+                                         ([31, 32, 33, 3000, 0, 64], 1000)])
+def test_plan_decode_head_pairs_small_and_ragged(lens, target):
+    """KV-head pairs on short, empty and ragged rows (single-page rows, a row of one
+    token, splits of one tile, more tasks than resident workgroups so that workgroups
+    loop over several pairs): bitwise the two-launch route, and the oracle within
+    tolerance."""
+    case = Case(lens, seed=31)
+    p = plan_params(8, 1, 64, target, policy=1)
+    expect, tasks_ref, _ = _two_launch(case, p, 64)
+    bufs = bufs_for(case, 64)
+    for rep in range(2):
+        out = run_plan_decode(case, bufs, p)
+        tasks, _ = read_plan(bufs)
+        assert np.array_equal(tasks, tasks_ref), rep
+        assert torch.equal(out, expect), rep
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"pairs {lens}")
     assert pkv.pkv_check_device_status(bufs.ws) == 0
