@@ -85,9 +85,9 @@ class Runner:
 
         self.torch, self.pkv = torch, pkv
         w = make_workload(name, seed=seed, steps=steps, hkv=hkv)
-        if not target_tasks:  # the cost model's rule for the first step's active rows
+        if not target_tasks:  # the cost model's rule for the first step's lengths
             from paper_2606_26666_amd import costmodel
-            target_tasks = costmodel.default_target(int(np.count_nonzero(w.lengths_at(0))), w.hkv, hq=w.hq)
+            target_tasks = costmodel.default_target(w.lengths_at(0), w.hkv, hq=w.hq)
         self.w = w = dataclasses.replace(w, target_tasks=target_tasks)
         self.dev = torch.device("cuda:0")
         shape = (w.num_pages, w.page_size, w.hkv, w.head_dim)

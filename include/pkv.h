@@ -179,7 +179,7 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
  * workgroup starts loading the task listed at its own index while the planner runs and
  * keeps those loads only if the new plan gives it the same pages. Any contents are
  * allowed (out-of-range records are ignored) and never change a result.
- * With G in {4, 8}, Hkv even and params->target_tasks at least twice the workgroups the
+ * With G = 4, Hkv even and params->target_tasks at least twice the workgroups the
  * device holds at once (512 on MI355X), each workgroup runs two tasks together: KV heads
  * g and g + 1 of one split, whose slices of each token are adjacent (its hint is then
  * the record at twice its index). This changes only which workgroup computes what.

@@ -79,29 +79,37 @@ def slot_bytes(G: int, d: int = 128) -> int:
 
 
 def head_pairs(hq: int, hkv: int) -> bool:
-    """Whether the one-launch route can run KV heads g and g + 1 in one workgroup: the
-    matrix-core task body (G = 4 or 8) with an even KV-head count. The library does so
-    when the task target is at least two tasks per resident workgroup."""
-    return hkv > 0 and hq % hkv == 0 and hq // hkv in (4, 8) and hkv % 2 == 0
+    """Whether the one-launch route runs KV heads g and g + 1 in one workgroup: G = 4
+    (the matrix-core task body; at G = 8 a pair's merge needs two rounds of loads and
+    pairs measured 11% slower on the B8 traces) with an even KV-head count. The library
+    does so when the task target is at least two tasks per resident workgroup."""
+    return hkv > 0 and hq % hkv == 0 and hq // hkv == 4 and hkv % 2 == 0
 
 
-def default_target(active_rows: int, hkv: int, cus: int = CUS, per_row: int = SPLITS_PER_ROW_HEAD,
-                   hq: int = 32) -> int:
-    """Task target of the workqueue planner (Sec. 3.5's split choice) for a step with
-    `active_rows` non-empty rows: one task per compute unit, raised so that each KV head
-    has room for `per_row` splits per active row. With many KV heads a fixed target of one
-    task per compute unit leaves a ragged batch one or two splits per row and head, and
-    the longest row's task sets the step (measured on MI355X: B8 traces at Hkv = 32 run
-    24-47% faster at 1024 tasks than at 256).
+PAIR_MAX_SPLITS = 24  # splits per (row, KV head) up to which KV-head pairs pay
 
-    Two tasks per compute unit when KV-head pairs apply and the batch has at least 64
-    (row, KV head) pairs, i.e. at most 8 splits per row and head: each workgroup then
-    streams two heads' slices of every token, which evens out the per-head read rates,
-    and its last arriver merges both heads' few states in one pass (measured: B8 traces
-    4-6% faster than at 256 tasks). With fewer rows the pair merges grow past one round of
-    loads and cost more than the balance gains (B1 and B4: 256 tasks are best)."""
-    base = max(cus, per_row * hkv * max(1, int(active_rows)))
-    if head_pairs(hq, hkv) and hkv * int(active_rows) >= 64:
+
+def default_target(lens, hkv: int, cus: int = CUS, per_row: int = SPLITS_PER_ROW_HEAD, hq: int = 32) -> int:
+    """Task target of the workqueue planner (Sec. 3.5's split choice) for a step over the
+    lengths `lens`: one task per compute unit, raised so that each KV head has room for
+    `per_row` splits per active row. With many KV heads a fixed target of one task per
+    compute unit leaves a ragged batch one or two splits per row and head, and the longest
+    row's task sets the step (measured on MI355X: B8 traces at Hkv = 32 run 24-47% faster
+    at 1024 tasks than at 256).
+
+    Two tasks per compute unit where KV-head pairs apply and, at that target, the longest
+    row would get at most 24 splits per KV head (its share of the step's tokens times the
+    2 * cus / Hkv splits per head): each workgroup then streams two heads' slices of every
+    token, which evens out the per-head read rates, and a pair's last arriver merges both
+    heads' few states in one round of loads. Measured at Hkv = 8: the B8 traces (longest
+    row 20-35% of the tokens, at most 21 splits) run 3-6% faster than at 256 tasks; B4
+    bimodal (31-35 splits) and B1 (64 splits) run 5% and 11% slower, the pair merges
+    outgrowing the balance gain."""
+    lens = np.asarray(lens, dtype=np.int64).reshape(-1)
+    active = int(np.count_nonzero(lens))
+    base = max(cus, per_row * hkv * max(1, active))
+    total = int(lens.sum())
+    if head_pairs(hq, hkv) and total > 0 and 2 * cus * int(lens.max()) <= PAIR_MAX_SPLITS * hkv * total:
         return max(base, 2 * cus)
     return base
 

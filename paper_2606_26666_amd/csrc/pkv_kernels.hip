@@ -15,8 +15,8 @@
 // v_dot2_f32_f16 completed by a 16-lane DPP butterfly, and runs an online softmax per
 // lane row (m, l, acc[G][8 dims]) in fp32. Each ends with an LDS combine of the W wave
 // states in a fixed order. The one-launch route can give a workgroup KV heads g and
-// g + 1 of one split instead (MfmaTask with NH = 2, one page in flight per head), which
-// balances the per-head read rates across workgroups.
+// g + 1 of one split instead (MfmaTask with NH = 2, one page in flight per head; G = 4),
+// which balances the per-head read rates across workgroups.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -1513,8 +1513,10 @@ hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t 
     return launch(split_kernel<G, W, true, false>, grid < resident ? grid : resident, W * 64, s, start, stop, a);
   }
   if (mode == 3) {
-    // KV-head pairs when the task target gives every resident workgroup two tasks
-    if constexpr (mfma_task<G>()) {
+    // KV-head pairs when the task target gives every resident workgroup two tasks (G = 4:
+    // at G = 8 the pair merge needs two rounds of loads and the pairs ran 11% slower on
+    // the B8 traces)
+    if constexpr (G == 4) {
       static const int resident2 = resident_blocks((const void*)split_kernel<G, W, true, true, 2>, W * 64);
       if (a.Hkv % 2 == 0 && a.plan.target_tasks >= 2 * resident2) {
         const int pairs = grid / 2;

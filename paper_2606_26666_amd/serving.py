@@ -138,7 +138,7 @@ class Engine:
             self.q.mul_(1.0 / np.sqrt(self.d))
         self.lens.copy_(torch.from_numpy(self.lens_host))
         if not self.fixed_target:
-            self.params.target_tasks = costmodel.default_target(idx.size, self.hkv, hq=self.hq)
+            self.params.target_tasks = costmodel.default_target(self.lens_host[idx], self.hkv, hq=self.hq)
         b = self.bufs
         _b.pkv_plan_decode(self.q, self.k, self.v, self.bt, self.lens, self.params, b.tasks, b.split_offsets,
                            b.num_tasks, 1.0, self.out, b.ws)

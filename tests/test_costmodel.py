@@ -89,22 +89,28 @@ def test_committed_calibration_loads():
 def test_default_target_rule():
     """One task per compute unit unless the KV heads need room for 4 splits per active
     row (the measured optimum of every G and trace in the split sweep), and two per
-    compute unit where KV-head pairs run with at most 8 splits per row and head."""
-    assert cm.default_target(1, 8) == 256            # B1, G = 4
-    assert cm.default_target(8, 8) == 512            # B8, G = 4: KV-head pairs, two tasks per CU
-    assert cm.default_target(4, 8) == 256            # B4, G = 4: pair merges would grow
-    assert cm.default_target(16, 4) == 512           # 16 rows, G = 8: pairs
-    assert cm.default_target(8, 8, hq=8) == 256      # G = 1 body runs one head
-    assert cm.head_pairs(32, 8) and cm.head_pairs(32, 4) and not cm.head_pairs(32, 16)
+    compute unit where KV-head pairs run and the longest row would get at most 24 splits
+    per KV head at that target."""
+    b1, b4 = [32768], [1500, 20000, 0, 30000]
+    b8 = [300, 20000, 1800, 31000, 700, 25000, 1200, 17000]   # longest row 32% of the tokens
+    assert cm.default_target(b1, 8) == 256           # B1, G = 4: one row
+    assert cm.default_target(b8, 8) == 512           # B8, G = 4: KV-head pairs, two tasks per CU
+    assert cm.default_target(b4, 8) == 256           # B4, G = 4: longest row 58% of the tokens
+    assert cm.default_target(b8, 4) == 256           # B8, G = 8: one head per workgroup
+    assert cm.default_target([1000] * 16, 8) == 512  # 16 even rows, G = 4: 4 splits per row
+    assert cm.default_target(b8, 8, hq=8) == 256     # G = 1 body runs one head
+    share = [1000] * 8
+    share[0] = 4200                                  # 3/8 of the tokens: exactly 24 splits at Hkv = 8
+    assert cm.default_target(share, 8) == 512 and cm.default_target([4201] + share[1:], 8) == 256
+    assert cm.head_pairs(32, 8) and not cm.head_pairs(32, 4) and not cm.head_pairs(32, 16)
     assert not cm.head_pairs(12, 3)                  # odd KV-head count
-    assert cm.default_target(8, 4) == 256            # B8, G = 8
-    assert cm.default_target(8, 16) == 512           # B8, G = 2
-    assert cm.default_target(8, 32) == 1024          # B8, G = 1
-    assert cm.default_target(4, 32) == 512           # B4, G = 1
-    assert cm.default_target(1, 32) == 256           # B1, G = 1
-    assert cm.default_target(0, 8) == 256            # an idle step still gets a valid target
+    assert cm.default_target(b8, 16) == 512          # B8, G = 2
+    assert cm.default_target(b8, 32) == 1024         # B8, G = 1
+    assert cm.default_target(b4[:3] + [9000], 32) == 384  # three active rows, G = 1: 4 * 32 * 3
+    assert cm.default_target(b1, 32) == 256          # B1, G = 1
+    assert cm.default_target([0, 0], 8) == 256       # an idle step still gets a valid target
     # the planner never exceeds the task buffer whatever the target: B * Hkv * split_max
     lens = [20000, 300, 0, 9000]
-    p = params(target=cm.default_target(3, 32), smin=1, smax=64, policy=1, hkv=32)
+    p = params(target=cm.default_target(lens, 32), smin=1, smax=64, policy=1, hkv=32)
     _, _, n = pkv.pkv_plan_host(lens, p, 2000, with_tasks=False)
     assert n <= p.target_tasks and n <= len(lens) * 32 * 64

@@ -308,7 +308,7 @@ def test_plan_decode_gqa_mappings_full_size(name, hkv):
     loop over several tasks after their speculative first one)."""
     from paper_2606_26666_amd import costmodel
     case, w = Case.from_workload(name, hkv=hkv)
-    target = costmodel.default_target(int(np.count_nonzero(case.lens)), w.hkv)
+    target = costmodel.default_target(case.lens, w.hkv)
     p = plan_params(w.hkv, w.split_min, w.split_max, target, w.tile_tokens, policy=1)
     bufs = bufs_for(case, w.split_max)
     out = run_plan_decode(case, bufs, p)
@@ -448,11 +448,11 @@ def test_plan_decode_batch_above_one_wave():
                                              ("b8_zipf", 8, 1), ("b4_bimodal", 8, 1), ("b1", 4, 1),
                                              ("b8_bimodal", 4, 1)])
 def test_plan_decode_head_pairs_full_size(name, hkv, policy):
-    """Task target 512 on the benchmark lengths: the one-launch route runs KV heads g and
-    g + 1 of a split in one workgroup (G = 4 and G = 8). Each head's arithmetic is that of
-    a one-head task, so the output is bitwise the plan-kernel + fused-kernel route's at the
-    same plan, and within tolerance of the oracle; a repeated call (every workgroup
-    starting from its hint) is bitwise the same."""
+    """Task target 512 on the benchmark lengths: at G = 4 the one-launch route runs KV
+    heads g and g + 1 of a split in one workgroup (at G = 8 one head, two tasks per
+    workgroup). Each head's arithmetic is that of a one-head task, so the output is bitwise
+    the plan-kernel + fused-kernel route's at the same plan, and within tolerance of the
+    oracle; a repeated call (every workgroup starting from its hint) is bitwise the same."""
     case, w = Case.from_workload(name, hkv=hkv)
     p = plan_params(w.hkv, w.split_min, w.split_max, 512, w.tile_tokens, policy=policy)
     expect, tasks_ref, offs_ref = _two_launch(case, p, w.split_max)
