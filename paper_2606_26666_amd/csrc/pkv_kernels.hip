@@ -1299,8 +1299,9 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
     if (wave_plan(a.plan)) {
       // Speculative start. Between decode steps a plan rarely changes (lengths grow by a
       // token), so while wave 0 runs the planner, each wave begins and primes the task
-      // listed at this workgroup's index in the task list left by the previous launch
-      // (the task it ran then): a hint, read with agent-scope loads because workgroup 0
+      // listed at this workgroup's index (NH = 2: the pair's first task, at twice the
+      // index) in the task list left by the previous launch (the task it ran then): a
+      // hint, read with agent-scope loads because workgroup 0
       // rewrites the list meanwhile. A record is used only if it names a task inside the
       // batch's bounds (the buffer may hold anything on the first call), and the begun
       // loads are kept only if the new plan gives this workgroup a task they cover;
