@@ -182,6 +182,54 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
   const int my_hh = myh / G, my_h = myh % G;
   auto soff = [&](int s, int hh) { return (slot0 + s * stride + hh) * SB; };
 
+  // One run of splits or fewer, and a float4 column of the output per thread: each
+  // thread loads every state's m, l and acc column of its head itself, so the maximum,
+  // the weights and both sums are formed in its registers, with no exchange between
+  // threads and no barrier. The operations and their order are those of the general
+  // path below (which, for one run, adds each sum once to a zero), so both paths round
+  // identically.
+  if (nsplit <= kMergeRun && E4 <= NT) {
+    if (tid < E4) {
+      const int hh = tid / E4H;
+      const int e4l = tid - hh * E4H;
+      const int h = (e4l * 4) / D;
+      float mq[kMergeRun], lq[kMergeRun];
+      v4f vq[kMergeRun];
+#pragma unroll
+      for (int u = 0; u < kMergeRun; ++u) {  // a state that does not exist reads as zero
+        const int off = u < nsplit ? soff(u, hh) : kOutOfRange;
+        mq[u] = ld_state<COHERENT>(pr, off + (G * D + h) * 4);
+        lq[u] = ld_state<COHERENT>(pr, off + (G * D + G + h) * 4);
+        vq[u] = ld_state4<COHERENT>(pr, off + e4l * 16);
+      }
+      float M = kNegInf, bd = 0.0f;
+#pragma unroll
+      for (int u = 0; u < kMergeRun; ++u) {
+        M = fmaxf(M, u < nsplit ? mq[u] : kNegInf);
+        bd = fmaxf(bd, lq[u] < 0.0f ? 1.0f : 0.0f);
+      }
+      const float Mref = (M == kNegInf) ? 0.0f : M;
+      v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      float lacc = 0.0f;
+#pragma unroll
+      for (int u = 0; u < kMergeRun; ++u) {
+        const float w = u < nsplit ? ex2(mq[u] - Mref) : 0.0f;
+        const float lw = u < nsplit ? lq[u] : 0.0f;
+        acc.x = __builtin_fmaf(w, vq[u].x, acc.x);
+        acc.y = __builtin_fmaf(w, vq[u].y, acc.y);
+        acc.z = __builtin_fmaf(w, vq[u].z, acc.z);
+        acc.w = __builtin_fmaf(w, vq[u].w, acc.w);
+        lacc = __builtin_fmaf(w, lw, lacc);
+      }
+      const float L = 0.0f + lacc;
+      const bool zero = M == kNegInf || bd != 0.0f;
+      const float A[4] = {0.0f + acc.x, 0.0f + acc.y, 0.0f + acc.z, 0.0f + acc.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) out_grp[tid * 4 + j] = f32_to_f16_bits(zero ? 0.0f : A[j] / L);
+    }
+    return;
+  }
+
   float mv[KPT], lv[KPT];
   auto load_ml = [&](int s0, int cnt) {
 #pragma unroll
