@@ -114,3 +114,21 @@ def test_default_target_rule():
     p = params(target=cm.default_target(lens, 32), smin=1, smax=64, policy=1, hkv=32)
     _, _, n = pkv.pkv_plan_host(lens, p, 2000, with_tasks=False)
     assert n <= p.target_tasks and n <= len(lens) * 32 * 64
+
+
+@pytest.mark.parametrize("name,expect", [("b1", 256), ("b8_bimodal", 512), ("b8_uniform", 512),
+                                         ("b8_zipf", 512), ("b4_bimodal", 256)])
+def test_default_target_on_benchmark_traces(name, expect):
+    """The targets the benchmark runs with at its main seed: KV-head pairs (512 tasks) on
+    the B8 traces, one head per workgroup (256) for B1 and B4; and the longest row's
+    split count at the chosen target stays within the pair limit where pairs run."""
+    from oracle.plan import PlanParams, ref_plan
+    from workloads import make_workload
+    w = make_workload(name, seed=20260623)
+    lens = w.lengths_at(0)
+    target = cm.default_target(lens, w.hkv, hq=w.hq)
+    assert target == expect
+    _, offs, _ = ref_plan(lens, PlanParams(split_min=w.split_min, split_max=w.split_max, target_tasks=target,
+                                           policy=1, num_kv_heads=w.hkv))
+    if target == 512:
+        assert int(np.diff(offs).max()) <= cm.PAIR_MAX_SPLITS
