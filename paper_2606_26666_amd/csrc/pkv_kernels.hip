@@ -214,12 +214,12 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
 #pragma unroll
       for (int u = 0; u < kMergeRun; ++u) {
         const float w = u < nsplit ? ex2(mq[u] - Mref) : 0.0f;
-        const float lw = u < nsplit ? lq[u] : 0.0f;
+        const float lu = u < nsplit ? lq[u] : 0.0f;
         acc.x = __builtin_fmaf(w, vq[u].x, acc.x);
         acc.y = __builtin_fmaf(w, vq[u].y, acc.y);
         acc.z = __builtin_fmaf(w, vq[u].z, acc.z);
         acc.w = __builtin_fmaf(w, vq[u].w, acc.w);
-        lacc = __builtin_fmaf(w, lw, lacc);
+        lacc = __builtin_fmaf(w, lu, lacc);
       }
       const float L = 0.0f + lacc;
       const bool zero = M == kNegInf || bd != 0.0f;
@@ -638,8 +638,8 @@ struct ValuTask {
 //   O^T[128 x 16] += V_page^T[128 x 16 tokens] . P^T[16 tokens x 16]   (16 x mfma 16x16x16 f16:
 //                                                                      P as hi + lo halves)
 // Lane (grp, col) = (lane / 16, lane % 16):
-//   K operand   token col, dims [32 kb + 8 grp, +8): one 16-byte load per kb, native layout
-//   Q operand   head col, dims [32 kb + 8 grp, +8) (zero for col >= G), loaded once
+//   K operand   token col, dims [32 c + 8 grp, +8): one 16-byte load per c, native layout
+//   Q operand   head col, dims [32 c + 8 grp, +8) (zero for col >= G), loaded once
 //   scores      tokens 4 grp + r (r = 0..3) of head col, which is also the P operand
 //   V operand   dims 16 db + col, tokens 4 grp + r: V is staged token-major in LDS and
 //               read back transposed with ds_read_b64_tr_b16 (within 16 lanes, lane i
@@ -690,9 +690,9 @@ struct MfmaTask {
     for (int hh = 0; hh < NH; ++hh) {
       const uint16_t* qh = a.q + ((size_t)row * a.Hq + (size_t)(g + hh) * G + (hv ? col : 0)) * D;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
+      for (int c = 0; c < 4; ++c) {
         const v4u z = {0u, 0u, 0u, 0u};
-        qb[hh][kb] = hv ? *reinterpret_cast<const v4u*>(qh + kb * 32 + 8 * grp) : z;
+        qb[hh][c] = hv ? *reinterpret_cast<const v4u*>(qh + c * 32 + 8 * grp) : z;
       }
     }
     ids = lane < npw ? a.block_table[(size_t)row * a.max_pages_per_row + first + lane * W] : 0;
@@ -714,7 +714,7 @@ struct MfmaTask {
     const size_t tok_stride = (size_t)a.Hkv * D;  // halves between consecutive tokens
     const size_t page_stride = (size_t)P * tok_stride;
     const int tok_b = (int)(tok_stride * 2);
-    const int k_off = col * tok_b + (g + hh) * D * 2 + grp * 16;  // + 64 kb
+    const int k_off = col * tok_b + (g + hh) * D * 2 + grp * 16;  // + 64 c
     const int v_off = grp * tok_b + (g + hh) * D * 2 + col * 16;  // + 4 i tok_b
     const bool ok = phys >= 0 && phys < a.num_pages;
     bad |= live && !ok;
@@ -723,7 +723,7 @@ struct MfmaTask {
     const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, page_bytes);
     const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, page_bytes);
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) kr[kb] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, k_off, kb * 64, 0);
+    for (int c = 0; c < 4; ++c) kr[c] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, k_off, c * 64, 0);
 #pragma unroll
     for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, v_off, i * 4 * tok_b, 0);
   }
@@ -772,8 +772,8 @@ struct MfmaTask {
       const bool tail = pg * P + P > t1;  // the row's last, partial page
       v4f sc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[kb]), __builtin_bit_cast(h8v, qh[kb]),
+      for (int c = 0; c < 4; ++c)
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[c]), __builtin_bit_cast(h8v, qh[c]),
                                                     sc, 0, 0, 0);
       // stage V token-major; rows past t1 are zeroed (their p is 0, but 0 * NaN is not)
 #pragma unroll
