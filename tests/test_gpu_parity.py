@@ -486,3 +486,22 @@ def test_plan_decode_head_pairs_small_and_ragged(lens, target):
         assert torch.equal(out, expect), rep
     assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"pairs {lens}")
     assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (12, 3), (64, 16)])
+def test_plan_decode_head_pairs_other_head_counts(hq, hkv):
+    """Task target 512 at G = 4 with other KV-head counts: two KV heads (one pair per
+    split), an odd count (no pairs: one head per workgroup), and sixteen. Bitwise the
+    two-launch route, and the oracle within tolerance."""
+    case = Case([3000, 0, 700, 17, 9000], hq=hq, hkv=hkv, seed=33)
+    p = plan_params(hkv, 1, 64, 512, policy=1)
+    expect, tasks_ref, _ = _two_launch(case, p, 64)
+    bufs = bufs_for(case, 64)
+    for rep in range(2):
+        out = run_plan_decode(case, bufs, p)
+        tasks, _ = read_plan(bufs)
+        assert np.array_equal(tasks, tasks_ref), rep
+        assert torch.equal(out, expect), rep
+    assert np.array_equal(tasks, oracle_plan(case, p)[0])
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"pairs hq={hq} hkv={hkv}")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
