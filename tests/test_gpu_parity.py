@@ -505,3 +505,41 @@ def test_plan_decode_head_pairs_other_head_counts(hq, hkv):
     assert np.array_equal(tasks, oracle_plan(case, p)[0])
     assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"pairs hq={hq} hkv={hkv}")
     assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+def _random_config(seed):
+    r = np.random.Generator(np.random.PCG64(seed))
+    hq, hkv = [(32, 8), (32, 4), (32, 16), (32, 32), (8, 2), (16, 4)][seed % 6]
+    B = int(r.integers(1, 41))
+    kind = r.integers(0, 4, size=B)  # empty, one page or less, medium, long
+    lens = np.where(kind == 0, 0, np.where(kind == 1, r.integers(1, 17, size=B),
+                    np.where(kind == 2, r.integers(17, 2000, size=B), r.integers(2000, 9000, size=B))))
+    budget = 480000 // hkv  # tokens: keep the pools and the fp64 oracle small
+    if lens.sum() > budget:
+        lens = (lens * (budget / lens.sum())).astype(np.int64)
+    smin = int(r.integers(1, 9))
+    smax = int(r.integers(smin, 65))
+    target = int(r.choice([64, 256, 512, 700, 2048]))
+    return lens.astype(np.int32), hq, hkv, smin, smax, target, int(seed % 2)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_plan_decode_random_configurations(seed):
+    """Seeded random batches (1-40 rows of empty, single-page, medium and long lengths),
+    query/KV head counts G = 1, 2, 4, 8, split bounds, task targets from 64 to 2048 (so
+    one or several tasks per workgroup, and KV-head pairs at G = 4 from 512) and both
+    split policies: the one-launch route is bitwise the plan + fused route, its task list
+    is the oracle's, and its output is within tolerance of the oracle."""
+    lens, hq, hkv, smin, smax, target, policy = _random_config(seed)
+    case = Case(lens, hq=hq, hkv=hkv, seed=100 + seed)
+    p = plan_params(hkv, smin, smax, target, policy=policy)
+    expect, tasks_ref, offs_ref = _two_launch(case, p, smax)
+    bufs = bufs_for(case, smax)
+    out = run_plan_decode(case, bufs, p)
+    tasks, offs = read_plan(bufs)
+    ref_t, ref_o, _ = oracle_plan(case, p)
+    assert np.array_equal(tasks, ref_t) and np.array_equal(offs, ref_o)
+    assert np.array_equal(tasks, tasks_ref) and np.array_equal(offs, offs_ref)
+    assert torch.equal(out, expect), (seed, hq, hkv, target, policy)
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"random config {seed}")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
