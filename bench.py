@@ -290,6 +290,13 @@ def calibrate(pkv, torch, flush_bufs, reps=10, launches=200):
     return {"beta_read_gbs": beta, "launch_gap_us": lam}
 
 
+def head_pairs(hq, hkv, target):
+    """Whether the one-launch kernel runs KV-head pairs: G = 4, even Hkv and at least two
+    tasks per resident workgroup (one workgroup per compute unit)."""
+    from paper_2606_26666_amd import costmodel
+    return costmodel.head_pairs(hq, hkv) and target >= 2 * costmodel.CUS
+
+
 def summarize(runner, m):
     w = runner.w
     tokens = w.batch * len(m["step_ms"])
@@ -314,6 +321,9 @@ def summarize(runner, m):
         "decode_gbs": achieved,
         "step_gbs": float(np.mean(alg)) / (float(np.mean(m["step_ms"])) / 1e3) / 1e9,
         "tasks_per_step": float(np.mean(m["ntasks"])),
+        "task_target": int(w.target_tasks),
+        "kv_heads_per_workgroup": 2 if runner.route == "one-launch" and head_pairs(w.hq, w.hkv, w.target_tasks)
+                                  else 1,
         "launches_per_step": launches_per_step(runner),
         **route_counters(runner, m),
     }
