@@ -543,3 +543,31 @@ def test_plan_decode_random_configurations(seed):
     assert torch.equal(out, expect), (seed, hq, hkv, target, policy)
     assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"random config {seed}")
     assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("name", ["b1", "b8_bimodal"])
+def test_plan_decode_every_step_of_a_benchmark_run(name):
+    """Every decode step of a benchmark run at full size, as bench.py runs it (one
+    workspace, the task target of the cost model's rule for the first step's lengths,
+    lengths growing by one token per step, so every launch after the first starts from
+    the previous plan's hint, KV-head pairs on B8): each step bitwise the plan + fused
+    route and its task list the oracle's; the first and last steps within tolerance of
+    the oracle."""
+    from paper_2606_26666_amd import costmodel
+    case, w = Case.from_workload(name)
+    target = costmodel.default_target(w.lengths_at(0), w.hkv, hq=w.hq)
+    p = plan_params(w.hkv, w.split_min, w.split_max, target, w.tile_tokens, policy=1)
+    bufs = bufs_for(case, w.split_max)
+    for s in range(w.steps):
+        lens = w.lengths_at(s)
+        case.lens = lens
+        case.lens_dev = torch.from_numpy(lens).cuda()
+        expect, tasks_ref, _ = _two_launch(case, p, w.split_max)
+        out = run_plan_decode(case, bufs, p)
+        tasks, _ = read_plan(bufs)
+        assert np.array_equal(tasks, tasks_ref), s
+        assert torch.equal(out, expect), s
+        if s in (0, w.steps - 1):
+            assert np.array_equal(tasks, oracle_plan(case, p)[0]), s
+            assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, lens), f"{name} step {s}")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
