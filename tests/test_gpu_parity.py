@@ -571,3 +571,26 @@ def test_plan_decode_every_step_of_a_benchmark_run(name):
             assert np.array_equal(tasks, oracle_plan(case, p)[0]), s
             assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, lens), f"{name} step {s}")
     assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("target", [256, 512])
+def test_plan_decode_maximum_batch(target):
+    """The largest batch the one-launch route plans in-launch (1024 rows, a tenth of them
+    empty, 1-300 tokens each): thousands of tasks, so every workgroup loops over many
+    (one head, or KV-head pairs at 512); bitwise the two-launch route, the oracle's task
+    list, and the oracle within tolerance."""
+    r = np.random.Generator(np.random.PCG64(41))
+    lens = r.integers(1, 301, size=1024).astype(np.int32)
+    lens[r.permutation(1024)[:102]] = 0
+    case = Case(lens, seed=41)
+    p = plan_params(8, 1, 4, target, policy=1)
+    expect, tasks_ref, offs_ref = _two_launch(case, p, 4)
+    bufs = bufs_for(case, 4)
+    for rep in range(2):
+        out = run_plan_decode(case, bufs, p)
+        tasks, offs = read_plan(bufs)
+        assert np.array_equal(tasks, tasks_ref) and np.array_equal(offs, offs_ref), rep
+        assert torch.equal(out, expect), rep
+    assert np.array_equal(tasks, oracle_plan(case, p)[0])
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"B=1024 target {target}")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
