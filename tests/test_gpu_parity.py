@@ -594,3 +594,21 @@ def test_plan_decode_maximum_batch(target):
     assert np.array_equal(tasks, oracle_plan(case, p)[0])
     assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"B=1024 target {target}")
     assert pkv.pkv_check_device_status(bufs.ws) == 0
+
+
+@pytest.mark.parametrize("target", [8, 512])
+def test_plan_decode_one_split_per_long_row(target):
+    """One split per row (bounds (1, 1)) over rows of up to 40000 tokens: a task spans up
+    to 2500 pages, so each wave walks several blocks of 64 page ids (one head per
+    workgroup at target 8, KV-head pairs at 512). Bitwise the two-launch route and within
+    tolerance of the oracle."""
+    case = Case([40000, 13, 20001, 0, 5000], seed=43)
+    p = plan_params(8, 1, 1, target, policy=1)
+    expect, tasks_ref, _ = _two_launch(case, p, 1)
+    bufs = bufs_for(case, 1)
+    out = run_plan_decode(case, bufs, p)
+    tasks, _ = read_plan(bufs)
+    assert np.array_equal(tasks, tasks_ref) and np.array_equal(tasks, oracle_plan(case, p)[0])
+    assert torch.equal(out, expect)
+    assert_close(out, ref_decode(case.q, case.k, case.v, case.bt, case.lens), f"one split, target {target}")
+    assert pkv.pkv_check_device_status(bufs.ws) == 0
