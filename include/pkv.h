@@ -109,9 +109,11 @@ int32_t pkv_max_tasks(int32_t B, int32_t Hkv, int32_t split_max);
  * pkv_decode of a step must pass the same B. */
 size_t pkv_workspace_size(int32_t B, int32_t Hq, int32_t Hkv, int32_t d, int32_t max_tasks);
 
-/* Zero the workspace header and completion counters (enqueued on `stream`). Call once
- * after allocating a workspace; afterwards the library keeps the counters at zero
- * between calls and the error word is cleared by pkv_check_device_status. */
+/* Zero the workspace header and completion counters and record the counter count
+ * (B * Hkv) in the header (enqueued on `stream`). Call once after allocating a
+ * workspace; afterwards every call leaves the counters at zero, and
+ * pkv_check_device_status clears the error word and, when it finds error bits, re-zeroes
+ * the counters that a flagged call may have left short (see pkv_plan_decode). */
 int pkv_workspace_init(void* ws, size_t ws_bytes, int32_t B, int32_t Hkv, hipStream_t stream);
 
 /* Build the compact workqueue of Sec. 3.4 on the device (one kernel).
@@ -173,8 +175,12 @@ int pkv_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cac
  * result, and the first workgroup also writes tasks, split_offsets and num_tasks exactly
  * as pkv_plan writes them. Arguments as for pkv_plan and pkv_decode; the block table is
  * checked by the decode (not by the planner), B <= 1024, params->num_kv_heads == Hkv.
- * The completion counters must be zero at launch: pkv_workspace_init zeroes them and
- * every completed pkv_plan, pkv_decode or pkv_plan_decode call leaves them zero.
+ * The completion counters must be zero at launch: pkv_workspace_init zeroes them,
+ * and every completed pkv_plan, pkv_plan_decode or pkv_decode call leaves them zero,
+ * except a pkv_decode whose task list or split_offsets is not a plan of its seq_lens
+ * (PKV_DEVERR_TASK): such a call may leave counters short of their split count, and
+ * pkv_check_device_status re-zeroes them when it reports the error (for a workspace
+ * set up by pkv_workspace_init; pkv_plan also zeroes them).
  * The previous contents of `tasks` (for B <= 64) are read as a scheduling hint: each
  * workgroup starts loading the task listed at its own index while the planner runs and
  * keeps those loads only if the new plan gives it the same pages. Any contents are

@@ -29,33 +29,48 @@ int check_heads(int32_t Hq, int32_t Hkv, int32_t d, int* G) {
   return PKV_OK;
 }
 
+// Inputs and output of a decode call (the workspace is checked by check_ws).
 int check_pool(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t num_pages,
-               const int32_t* bt, int32_t maxp, const int32_t* seq_lens, int32_t B, uint16_t* out,
-               void* ws) {
-  if (!q || !k || !v || !bt || !seq_lens || !out || !ws) return PKV_ERR_INVALID_ARG;
+               const int32_t* bt, int32_t maxp, const int32_t* seq_lens, int32_t B, uint16_t* out) {
+  if (!q || !k || !v || !bt || !seq_lens || !out) return PKV_ERR_INVALID_ARG;
   if (B < 1 || num_pages < 1 || maxp < 1) return PKV_ERR_INVALID_ARG;
   if ((int64_t)maxp * kPageSize > INT32_MAX) return PKV_ERR_INVALID_ARG;
-  // 16-byte vector loads of Q/K/V, 4-byte output stores, 16-byte workspace rows
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 4) || !aligned(ws, 16))
-    return PKV_ERR_INVALID_ARG;
+  // 16-byte vector loads of Q/K/V, 4-byte output stores
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 4)) return PKV_ERR_INVALID_ARG;
   return PKV_OK;
+}
+
+// A caller's workspace: 16-byte rows.
+int check_ws(const void* ws) { return ws && aligned(ws, 16) ? PKV_OK : PKV_ERR_INVALID_ARG; }
+
+// Where a call's device error word, completion counters and partial-state slots live.
+struct Scratch {
+  unsigned* err;
+  int32_t* counters;
+  float* partials;
+};
+
+// The layout of a caller's workspace (pkv_workspace_size).
+Scratch ws_layout(void* ws, int32_t B, int32_t Hkv) {
+  char* w = static_cast<char*>(ws);
+  return Scratch{reinterpret_cast<unsigned*>(w), reinterpret_cast<int32_t*>(w + kWsHeaderBytes),
+                 reinterpret_cast<float*>(w + partials_offset(B, Hkv))};
 }
 
 DecodeArgs make_args(const uint16_t* q, const uint16_t* k, const uint16_t* v, int32_t num_pages,
                      const int32_t* bt, int32_t maxp, const int32_t* seq_lens, int32_t B, int32_t Hq,
-                     int32_t Hkv, float sm_scale, uint16_t* out, void* ws) {
+                     int32_t Hkv, float sm_scale, uint16_t* out, const Scratch& sc) {
   DecodeArgs a;
   std::memset(&a, 0, sizeof(a));
-  char* w = static_cast<char*>(ws);
   a.q = q;
   a.k = k;
   a.v = v;
   a.block_table = bt;
   a.seq_lens = seq_lens;
   a.out = out;
-  a.err = reinterpret_cast<unsigned*>(w);
-  a.counters = reinterpret_cast<int32_t*>(w + kWsHeaderBytes);
-  a.partials = reinterpret_cast<float*>(w + partials_offset(B, Hkv));
+  a.err = sc.err;
+  a.counters = sc.counters;
+  a.partials = sc.partials;
   a.num_pages = num_pages;
   a.max_pages_per_row = maxp;
   a.B = B;
@@ -65,13 +80,14 @@ DecodeArgs make_args(const uint16_t* q, const uint16_t* k, const uint16_t* v, in
   return a;
 }
 
+// Planner arguments; the error word and counters come from `sc`.
 int make_plan_args(const int32_t* seq_lens, const int32_t* block_table, int32_t B, int32_t max_pages_per_row,
                    int32_t num_pages, const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
-                   int32_t* split_offsets, int32_t* num_tasks, void* ws, size_t ws_bytes, PlanArgs* out) {
-  if (!seq_lens || !params || !tasks || !split_offsets || !num_tasks || !ws) return PKV_ERR_INVALID_ARG;
+                   int32_t* split_offsets, int32_t* num_tasks, const Scratch& sc, PlanArgs* out) {
+  if (!seq_lens || !params || !tasks || !split_offsets || !num_tasks) return PKV_ERR_INVALID_ARG;
   if (B < 1 || B > kMaxPlanBatch || max_pages_per_row < 1) return PKV_ERR_INVALID_ARG;
   if (block_table && num_pages < 1) return PKV_ERR_INVALID_ARG;
-  if (!aligned(ws, 16) || !aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
+  if (!aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
   const pkv_plan_params p = *params;
   if (p.page_size != kPageSize) return PKV_ERR_UNSUPPORTED;
   if (p.tile_tokens <= 0 || p.tile_tokens % p.page_size != 0) return PKV_ERR_UNSUPPORTED;
@@ -83,7 +99,6 @@ int make_plan_args(const int32_t* seq_lens, const int32_t* block_table, int32_t 
   const int32_t bound = pkv_max_tasks(B, p.num_kv_heads, p.split_max);
   if (bound < 0) return PKV_ERR_INVALID_ARG;
   if (max_tasks < bound) return PKV_ERR_WORKSPACE;
-  if (ws_bytes < partials_offset(B, p.num_kv_heads)) return PKV_ERR_WORKSPACE;
   PlanArgs& a = *out;
   std::memset(&a, 0, sizeof(a));
   a.seq_lens = seq_lens;
@@ -102,8 +117,8 @@ int make_plan_args(const int32_t* seq_lens, const int32_t* block_table, int32_t 
   a.max_tasks = max_tasks;
   a.split_offsets = split_offsets;
   a.num_tasks = num_tasks;
-  a.err = reinterpret_cast<unsigned*>(ws);
-  a.counters = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + kWsHeaderBytes);
+  a.err = sc.err;
+  a.counters = sc.counters;
   return PKV_OK;
 }
 
@@ -127,16 +142,20 @@ int pkv_workspace_init(void* ws, size_t ws_bytes, int32_t B, int32_t Hkv, hipStr
   if (!ws || B < 1 || Hkv < 1 || !aligned(ws, 16)) return PKV_ERR_INVALID_ARG;
   const size_t n = partials_offset(B, Hkv);
   if (ws_bytes < n) return PKV_ERR_WORKSPACE;
-  return from_hip(launch_zero(ws, n, stream));
+  if ((int64_t)B * Hkv > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  return from_hip(launch_ws_init(ws, n, (uint32_t)(B * Hkv), stream));
 }
 
 int pkv_plan(const int32_t* seq_lens, const int32_t* block_table, int32_t B, int32_t max_pages_per_row,
              int32_t num_pages, const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
              int32_t* split_offsets, int32_t* num_tasks, void* ws, size_t ws_bytes, hipStream_t stream) {
-  PlanArgs a;
-  const int st = make_plan_args(seq_lens, block_table, B, max_pages_per_row, num_pages, params, tasks, max_tasks,
-                                split_offsets, num_tasks, ws, ws_bytes, &a);
+  int st = check_ws(ws);
   if (st != PKV_OK) return st;
+  PlanArgs a;
+  st = make_plan_args(seq_lens, block_table, B, max_pages_per_row, num_pages, params, tasks, max_tasks,
+                      split_offsets, num_tasks, ws_layout(ws, B, 1), &a);
+  if (st != PKV_OK) return st;
+  if (ws_bytes < partials_offset(B, params->num_kv_heads)) return PKV_ERR_WORKSPACE;  // header + counters
   return from_hip(launch_plan(a, stream));
 }
 
@@ -145,8 +164,8 @@ int pkv_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t*
                      int32_t Hq, int32_t Hkv, int32_t d, const pkv_task* tasks, const int32_t* split_offsets,
                      const int32_t* num_tasks, int32_t max_tasks, float sm_scale, int32_t flags, uint16_t* out,
                      void* ws, size_t ws_bytes, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
-  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
-  if (st != PKV_OK) return st;
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out);
+  if (st != PKV_OK || (st = check_ws(ws)) != PKV_OK) return st;
   if (!tasks || !split_offsets || !num_tasks || !aligned(tasks, 4)) return PKV_ERR_INVALID_ARG;
   int G = 0;
   if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
@@ -156,7 +175,7 @@ int pkv_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t*
   if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, max_tasks)) return PKV_ERR_WORKSPACE;
   if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
-                           Hkv, sm_scale, out, ws);
+                           Hkv, sm_scale, out, ws_layout(ws, B, Hkv));
   a.tasks = tasks;
   a.split_offsets = split_offsets;
   a.num_tasks = num_tasks;
@@ -181,8 +200,8 @@ int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
                     int32_t Hq, int32_t Hkv, int32_t d, const int32_t* row_ids, int32_t n_rows, int32_t S,
                     int32_t tile_tokens, float sm_scale, uint16_t* out, void* ws, size_t ws_bytes,
                     hipStream_t stream) {
-  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
-  if (st != PKV_OK) return st;
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out);
+  if (st != PKV_OK || (st = check_ws(ws)) != PKV_OK) return st;
   int G = 0;
   if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
   if (S < 1 || S > kMaxSplits || !std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
@@ -198,7 +217,7 @@ int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
   if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, slots)) return PKV_ERR_WORKSPACE;
   if ((int64_t)slots * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
-                           Hkv, sm_scale, out, ws);
+                           Hkv, sm_scale, out, ws_layout(ws, B, Hkv));
   a.S = S;
   a.tile_tokens = tile_tokens;
   a.max_tasks = slots;
@@ -212,8 +231,8 @@ int pkv_decode_buckets(const uint16_t* q, const uint16_t* k_cache, const uint16_
                        const int32_t* host_seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
                        int32_t bucket_tokens, const pkv_plan_params* params, float sm_scale, uint16_t* out,
                        void* ws, size_t ws_bytes, hipStream_t stream, int32_t* launches) {
-  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
-  if (st != PKV_OK) return st;
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out);
+  if (st != PKV_OK || (st = check_ws(ws)) != PKV_OK) return st;
   int G = 0;
   if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
   if (!host_seq_lens || !params || bucket_tokens < 0 || !std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
@@ -267,9 +286,17 @@ int pkv_decode_buckets(const uint16_t* q, const uint16_t* k_cache, const uint16_
 int pkv_check_device_status(void* ws, hipStream_t stream, uint32_t* error_bits) {
   if (!ws) return PKV_ERR_INVALID_ARG;
   if (hipStreamSynchronize(stream) != hipSuccess) return PKV_ERR_HIP;
-  uint32_t bits = 0;
-  if (hipMemcpy(&bits, ws, sizeof(bits), hipMemcpyDeviceToHost) != hipSuccess) return PKV_ERR_HIP;
+  uint32_t hdr[3] = {0, 0, 0};
+  if (hipMemcpy(hdr, ws, sizeof(hdr), hipMemcpyDeviceToHost) != hipSuccess) return PKV_ERR_HIP;
+  const uint32_t bits = hdr[0];
   if (launch_zero(ws, sizeof(uint32_t), stream) != hipSuccess) return PKV_ERR_HIP;
+  // A flagged call may have skipped tasks before they were counted (a task list or
+  // split_offsets that is not a plan of this batch), leaving completion counters short
+  // of their split count. Every call has finished here, so the counters recorded by
+  // pkv_workspace_init are restored to zero for the next fused call.
+  if (bits && hdr[1] > 0 && (hdr[1] ^ kWsCheckKey) == hdr[2] &&
+      launch_zero(static_cast<char*>(ws) + kWsHeaderBytes, (size_t)hdr[1] * 4, stream) != hipSuccess)
+    return PKV_ERR_HIP;
   if (hipStreamSynchronize(stream) != hipSuccess) return PKV_ERR_HIP;
   if (error_bits) *error_bits = bits;
   return bits ? PKV_ERR_DEVICE : PKV_OK;
@@ -297,13 +324,18 @@ int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s
   return from_hip(launch_read(src, bytes, sink, stream));
 }
 
-int pkv_plan_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
-                          const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens,
-                          int32_t B, int32_t Hq, int32_t Hkv, int32_t d, const pkv_plan_params* params,
-                          pkv_task* tasks, int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks,
-                          float sm_scale, uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream,
-                          hipEvent_t start, hipEvent_t stop) {
-  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out, ws);
+}  // extern "C"
+
+namespace {
+
+// pkv_plan_decode: every check, then the one-launch kernel with its error word,
+// counters and slots at `sc`. `slot_bytes` is the room for partial-state slots.
+int plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B, int32_t Hq,
+                int32_t Hkv, int32_t d, const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+                int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out, const Scratch& sc,
+                size_t slot_bytes, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+  int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out);
   if (st != PKV_OK) return st;
   int G = 0;
   if ((st = check_heads(Hq, Hkv, d, &G)) != PKV_OK) return st;
@@ -312,18 +344,41 @@ int pkv_plan_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint
   if (params && params->num_kv_heads != Hkv) return PKV_ERR_INVALID_ARG;
   PlanArgs pa;
   if ((st = make_plan_args(seq_lens, nullptr, B, max_pages_per_row, num_pages, params, tasks, max_tasks,
-                           split_offsets, num_tasks, ws, ws_bytes, &pa)) != PKV_OK)
+                           split_offsets, num_tasks, Scratch{nullptr, nullptr, nullptr}, &pa)) != PKV_OK)
     return st;
-  if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, max_tasks)) return PKV_ERR_WORKSPACE;
-  if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  if ((int64_t)max_tasks * slot_floats(G) * 4 > (int64_t)slot_bytes) return PKV_ERR_WORKSPACE;
+  if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
+  pa.err = sc.err;
+  pa.counters = sc.counters;
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
-                           Hkv, sm_scale, out, ws);
+                           Hkv, sm_scale, out, sc);
   a.tasks = tasks;
   a.split_offsets = split_offsets;
   a.num_tasks = num_tasks;
   a.max_tasks = max_tasks;
   a.plan = pa;
   return from_hip(launch_decode(a, G, 3, max_tasks, stream, start, stop));
+}
+
+}  // namespace
+
+extern "C" {
+
+int pkv_plan_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                          const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens,
+                          int32_t B, int32_t Hq, int32_t Hkv, int32_t d, const pkv_plan_params* params,
+                          pkv_task* tasks, int32_t max_tasks, int32_t* split_offsets, int32_t* num_tasks,
+                          float sm_scale, uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop) {
+  int st = check_ws(ws);
+  if (st != PKV_OK) return st;
+  if (B < 1 || Hkv < 1) return PKV_ERR_INVALID_ARG;
+  const size_t slots_at = partials_offset(B, Hkv);
+  if (ws_bytes < slots_at) return PKV_ERR_WORKSPACE;
+  const Scratch sc = ws_layout(ws, B, Hkv);
+  return plan_decode(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq, Hkv, d, params,
+                     tasks, max_tasks, split_offsets, num_tasks, sm_scale, out, sc, ws_bytes - slots_at, stream,
+                     start, stop);
 }
 
 int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,

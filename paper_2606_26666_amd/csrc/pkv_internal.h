@@ -16,6 +16,11 @@ constexpr int kMaxFusedPlanBatch = 1024;
 constexpr int kMaxSplits = 65536;  // split_max and the rectangular S: keeps split bounds in 32 bits
 constexpr int kMaxRectRows = 64;  // rows a rectangular launch can name (kernel arguments)
 constexpr size_t kWsHeaderBytes = 256;
+// workspace header words: 0 device error bits, 1 completion-counter count (written by
+// pkv_workspace_init), 2 that count xor kWsCheckKey
+constexpr int kWsCountWord = 1;
+constexpr int kWsCheckWord = 2;
+constexpr uint32_t kWsCheckKey = 0x5A17C0DEu;
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // fp32 acc[G][d], m[G], l[G], padded to 16 bytes
@@ -69,6 +74,7 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStream_t s,
                          hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_ws_init(void* ws, size_t bytes, uint32_t counters, hipStream_t s);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s);
 

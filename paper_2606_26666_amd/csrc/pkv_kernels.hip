@@ -1510,6 +1510,13 @@ __global__ void zero_kernel(uint32_t* p, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = 0u;
 }
 
+// Workspace set-up: header and counters zeroed, then the counter count and its check
+// word recorded in header words 1 and 2 (read back by pkv_check_device_status).
+__global__ void ws_init_kernel(uint32_t* p, size_t n, uint32_t counters) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = i == kWsCountWord ? counters : (i == kWsCheckWord ? counters ^ kWsCheckKey : 0u);
+}
+
 __global__ __launch_bounds__(256) void copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     dst[i] = src[i];
@@ -1609,6 +1616,14 @@ hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
   size_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   hipLaunchKernelGGL(zero_kernel, dim3((unsigned)blocks), dim3(256), 0, s, (uint32_t*)p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_ws_init(void* ws, size_t bytes, uint32_t counters, hipStream_t s) {
+  const size_t n = bytes / 4;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(ws_init_kernel, dim3((unsigned)blocks), dim3(256), 0, s, (uint32_t*)ws, n, counters);
   return hipGetLastError();
 }
 

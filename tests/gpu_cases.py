@@ -11,6 +11,7 @@ from workloads.values import device_normal_f16, host_normal_f16, poison_unassign
 
 ABS_TOL = 2e-3   # max |out - ref|
 REL_TOL = 1e-2   # max |out - ref| / max |ref| (normwise; elementwise relative error is ill-posed near 0)
+MEAN_TOL = 3e-4  # mean |out - ref|, the paper's second correctness statistic (Sec. 3.6)
 DEV = "cuda"
 
 
@@ -96,16 +97,26 @@ def run_rect(case, bufs, S, tile=32, sm_scale=1.0, poison_ws=True, row_ids=None,
 
 
 def assert_close(out, ref, label=""):
-    """The parity bar: max abs error <= 2e-3 and normwise relative error <= 1e-2."""
+    """The parity bar: max abs error <= 2e-3, normwise relative error <= 1e-2 and mean
+    abs error < 3e-4."""
     o = out.float().cpu().numpy().astype(np.float64) if isinstance(out, torch.Tensor) else out
     assert np.all(np.isfinite(o)), f"{label}: non-finite output"
     err = np.abs(o - ref)
     amax = float(err.max()) if err.size else 0.0
+    mean = float(err.mean()) if err.size else 0.0
     scale = float(np.abs(ref).max()) if ref.size else 0.0
     rel = amax / scale if scale > 0 else amax
     assert amax <= ABS_TOL, f"{label}: max abs err {amax:.3e}"
     assert rel <= REL_TOL, f"{label}: normwise rel err {rel:.3e}"
+    assert mean < MEAN_TOL, f"{label}: mean abs err {mean:.3e}"
     return amax, rel
+
+
+def error_stats(out, ref):
+    """max |e|, mean |e| and the fraction within one fp16 ulp of fp16(ref)."""
+    o = out.float().cpu().numpy().astype(np.float64)
+    err = np.abs(o - ref)
+    return float(err.max()), float(err.mean()), ulp_fraction(out, ref)
 
 
 def ulp_fraction(out, ref):
