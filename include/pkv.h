@@ -16,6 +16,8 @@
  * Conventions shared by every call:
  *  - Device pointers are HIP device memory owned by the caller. The library never
  *    allocates or frees memory and never synchronizes, except pkv_check_device_status.
+ *    (pkv_plan_decode_noalloc keeps its counters and partial states in a fixed scratch
+ *    area of each device's memory that the loaded library holds.)
  *  - All work is enqueued on `stream` and is asynchronous. A nonzero return means
  *    nothing was enqueued.
  *  - Tensors are row-major and contiguous; fp16 buffers hold IEEE binary16 bit patterns
@@ -196,6 +198,29 @@ int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
                     const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
                     int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* pkv_plan_decode for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same launch, with
+ * the completion counters and partial-state slots in a scratch area the library holds in
+ * each device's memory (16 MiB per device that runs this call, held until the process
+ * ends) instead of a caller's workspace. The call allocates nothing and performs no
+ * memset; its first call on a device looks up the scratch's address and zeroes its
+ * counters with a small kernel on `stream`.
+ *   error_bits  device uint32 [1], OR-ed with the device error bits of pkv_plan_decode
+ *               (PKV_DEVERR_*); the caller zeroes it and reads it when it wishes
+ *   other arguments as for pkv_plan_decode
+ * Limits: B * Hkv <= 16384 and max_tasks * slot bytes <= 16 MiB - 64 KiB (slot bytes as
+ * in pkv_workspace_size: 2080 at G = 4, i.e. max_tasks <= 8034), else
+ * PKV_ERR_WORKSPACE with nothing enqueued. Every call on a device shares that device's
+ * scratch: calls that overlap in time on one device (different streams, or different
+ * host threads) race and give wrong results; calls in order on one stream are safe,
+ * whatever their sizes. Outputs are bit-identical to pkv_plan_decode's. */
+int pkv_plan_decode_noalloc(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                            int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                            const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                            const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+                            int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
+                            uint32_t* error_bits, hipStream_t stream);
 
 /* pkv_decode and pkv_plan_decode with kernel-execution timestamps, for measurement:
  * start is recorded when the call's first kernel begins executing and stop when its

@@ -30,6 +30,7 @@ from ._binding import (  # noqa: F401
     pkv_plan,
     pkv_plan_host,
     pkv_plan_decode,
+    pkv_plan_decode_noalloc,
     pkv_stream_copy,
     pkv_stream_read,
     pkv_workspace_init,

@@ -56,6 +56,8 @@ _SIGS = {
                                   _F32, _I32, _P, _P, _SZ, _P]),
     "pkv_plan_decode": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
                                        ctypes.POINTER(PlanParams), _P, _I32, _P, _P, _F32, _P, _P, _SZ, _P]),
+    "pkv_plan_decode_noalloc": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
+                                               ctypes.POINTER(PlanParams), _P, _I32, _P, _P, _F32, _P, _P, _P]),
     "pkv_decode_timed": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _P, _P,
                                         _I32, _F32, _I32, _P, _P, _SZ, _P, _P, _P]),
     "pkv_plan_decode_timed": (ctypes.c_int, [_P, _P, _P, _I32, _P, _I32, _P, _I32, _I32, _I32, _I32,
@@ -223,6 +225,25 @@ def pkv_plan_decode(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tenso
         _check("pkv_plan_decode", lib().pkv_plan_decode(*args))
     else:
         _check("pkv_plan_decode_timed", lib().pkv_plan_decode_timed(*args, *ev))
+
+
+def pkv_plan_decode_noalloc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                            block_table: torch.Tensor, seq_lens: torch.Tensor, params: PlanParams,
+                            tasks: torch.Tensor, split_offsets: torch.Tensor, num_tasks: torch.Tensor,
+                            sm_scale: float, out: torch.Tensor, error_bits: torch.Tensor, *, stream=None):
+    """pkv_plan_decode without a caller workspace: counters and partial states live in the
+    library's per-device scratch (see include/pkv.h). error_bits: int32 [1] device tensor
+    that device error bits are OR-ed into (the caller zeroes it)."""
+    B, Hq, d = q.shape
+    num_pages, _, Hkv, _ = k_cache.shape
+    _check("pkv_plan_decode_noalloc", lib().pkv_plan_decode_noalloc(
+        _dev(q, torch.float16, "q"), _dev(k_cache, torch.float16, "k_cache"),
+        _dev(v_cache, torch.float16, "v_cache"), num_pages, _dev(block_table, torch.int32, "block_table"),
+        block_table.shape[1], _dev(seq_lens, torch.int32, "seq_lens"), B, Hq, Hkv, d, ctypes.byref(params),
+        _dev(tasks, torch.int32, "tasks"), tasks.numel() // TASK_FIELDS,
+        _dev(split_offsets, torch.int32, "split_offsets"), _dev(num_tasks, torch.int32, "num_tasks"),
+        float(sm_scale), _dev(out, torch.float16, "out"), _dev(error_bits, torch.int32, "error_bits"),
+        _stream(stream)))
 
 
 def _host_i32(x) -> tuple:

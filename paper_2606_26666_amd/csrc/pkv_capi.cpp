@@ -328,13 +328,15 @@ int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s
 
 namespace {
 
-// pkv_plan_decode: every check, then the one-launch kernel with its error word,
-// counters and slots at `sc`. `slot_bytes` is the room for partial-state slots.
+// pkv_plan_decode and pkv_plan_decode_noalloc: every check, then the one-launch kernel
+// with its error word, counters and slots at `*sc`, or (sc == nullptr) in the library's
+// scratch of the current device with the error word `err`. `slot_bytes` is the room for
+// partial-state slots.
 int plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
                 const int32_t* block_table, int32_t max_pages_per_row, const int32_t* seq_lens, int32_t B, int32_t Hq,
                 int32_t Hkv, int32_t d, const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
-                int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out, const Scratch& sc,
-                size_t slot_bytes, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
+                int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out, const Scratch* sc,
+                unsigned* err, size_t slot_bytes, hipStream_t stream, hipEvent_t start, hipEvent_t stop) {
   int st = check_pool(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, out);
   if (st != PKV_OK) return st;
   int G = 0;
@@ -348,10 +350,18 @@ int plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_ca
     return st;
   if ((int64_t)max_tasks * slot_floats(G) * 4 > (int64_t)slot_bytes) return PKV_ERR_WORKSPACE;
   if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
-  pa.err = sc.err;
-  pa.counters = sc.counters;
+  Scratch at{};
+  if (sc) {
+    at = *sc;
+  } else {  // every check has passed: only now is the device touched
+    char* base = nullptr;
+    if (static_scratch(stream, &base) != hipSuccess) return PKV_ERR_HIP;
+    at = Scratch{err, reinterpret_cast<int32_t*>(base), reinterpret_cast<float*>(base + kScratchCounterBytes)};
+  }
+  pa.err = at.err;
+  pa.counters = at.counters;
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
-                           Hkv, sm_scale, out, sc);
+                           Hkv, sm_scale, out, at);
   a.tasks = tasks;
   a.split_offsets = split_offsets;
   a.num_tasks = num_tasks;
@@ -377,8 +387,22 @@ int pkv_plan_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint
   if (ws_bytes < slots_at) return PKV_ERR_WORKSPACE;
   const Scratch sc = ws_layout(ws, B, Hkv);
   return plan_decode(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq, Hkv, d, params,
-                     tasks, max_tasks, split_offsets, num_tasks, sm_scale, out, sc, ws_bytes - slots_at, stream,
-                     start, stop);
+                     tasks, max_tasks, split_offsets, num_tasks, sm_scale, out, &sc, nullptr, ws_bytes - slots_at,
+                     stream, start, stop);
+}
+
+int pkv_plan_decode_noalloc(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                            int32_t num_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                            const int32_t* seq_lens, int32_t B, int32_t Hq, int32_t Hkv, int32_t d,
+                            const pkv_plan_params* params, pkv_task* tasks, int32_t max_tasks,
+                            int32_t* split_offsets, int32_t* num_tasks, float sm_scale, uint16_t* out,
+                            uint32_t* error_bits, hipStream_t stream) {
+  if (!error_bits || !aligned(error_bits, 4)) return PKV_ERR_INVALID_ARG;
+  if (B < 1 || Hkv < 1) return PKV_ERR_INVALID_ARG;
+  if ((int64_t)B * Hkv > kScratchCounters) return PKV_ERR_WORKSPACE;
+  return plan_decode(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq, Hkv, d, params,
+                     tasks, max_tasks, split_offsets, num_tasks, sm_scale, out, nullptr, error_bits,
+                     kScratchBytes - kScratchCounterBytes, stream, nullptr, nullptr);
 }
 
 int pkv_plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,

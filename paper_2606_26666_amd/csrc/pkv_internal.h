@@ -21,6 +21,12 @@ constexpr size_t kWsHeaderBytes = 256;
 constexpr int kWsCountWord = 1;
 constexpr int kWsCheckWord = 2;
 constexpr uint32_t kWsCheckKey = 0x5A17C0DEu;
+// library-held scratch of pkv_plan_decode_noalloc, per device: counters for up to
+// kScratchCounters (row, KV head) pairs, then partial-state slots
+constexpr size_t kScratchBytes = size_t(16) << 20;
+constexpr int kScratchCounters = 16384;
+constexpr size_t kScratchCounterBytes = size_t(kScratchCounters) * 4;
+constexpr int kMaxDevices = 64;
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // fp32 acc[G][d], m[G], l[G], padded to 16 bytes
@@ -75,6 +81,9 @@ hipError_t launch_decode(const DecodeArgs& a, int G, int mode, int grid, hipStre
                          hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_ws_init(void* ws, size_t bytes, uint32_t counters, hipStream_t s);
+// device address of the current device's library-held scratch; the first call on a
+// device zeroes its counters on stream s
+hipError_t static_scratch(hipStream_t s, char** base);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s);
 

@@ -20,6 +20,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "pkv_internal.h"
 
 namespace pkv {
@@ -1625,6 +1627,35 @@ hipError_t launch_ws_init(void* ws, size_t bytes, uint32_t counters, hipStream_t
   if (blocks > 4096) blocks = 4096;
   hipLaunchKernelGGL(ws_init_kernel, dim3((unsigned)blocks), dim3(256), 0, s, (uint32_t*)ws, n, counters);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------
+// Library-held scratch for pkv_plan_decode_noalloc: completion counters, then partial-
+// state slots. Each device holds its own copy; host code reaches it only through the
+// device address returned by hipGetSymbolAddress, taken once per device.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_scratch(hipStream_t s, char** base) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if ((e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    // counters start at zero; every completed call leaves them at zero
+    if ((e = launch_zero(ptr, kScratchCounterBytes, s)) != hipSuccess) return e;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *base = static_cast<char*>(g_scratch_ptr[dev]);
+  return hipSuccess;
 }
 
 hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s) {

@@ -158,6 +158,35 @@ def test_plan_decode_validation():
     assert pd(ws_bytes=4096) == pkv.PKV_ERR_WORKSPACE
 
 
+def test_plan_decode_noalloc_validation():
+    """The entry point without a workspace rejects, before touching any device, what
+    pkv_plan_decode rejects, a missing error word, and sizes beyond its scratch: B * Hkv
+    above 16384 completion counters, or more slots than 16 MiB - 64 KiB holds."""
+    L = lib()
+
+    def pd(**kw):
+        a = dict(B=2, hq=32, hkv=8, d=128, params=b.PlanParams(16, 32, 8, 16, 64, 512), max_tasks=2 * 8 * 64,
+                 err=FAKE)
+        a.update(kw)
+        return L.pkv_plan_decode_noalloc(FAKE, FAKE, FAKE, 100, FAKE, 10, FAKE, a["B"], a["hq"], a["hkv"], a["d"],
+                                         ctypes.byref(a["params"]), FAKE, a["max_tasks"], FAKE, FAKE, 1.0, FAKE,
+                                         a["err"], None)
+    assert pd(err=0) == pkv.PKV_ERR_INVALID_ARG
+    assert pd(err=FAKE + 2) == pkv.PKV_ERR_INVALID_ARG
+    assert pd(B=600, hkv=32, params=b.PlanParams(16, 32, 32, 1, 1, 512),
+              max_tasks=600 * 32) == pkv.PKV_ERR_WORKSPACE                    # 19200 counters > 16384
+    assert pd(B=1000, max_tasks=1000 * 8 * 64) == pkv.PKV_ERR_WORKSPACE     # 512000 slots > the scratch's
+    assert pd(B=1100, params=b.PlanParams(16, 32, 8, 1, 1, 512), max_tasks=1100 * 8) == pkv.PKV_ERR_UNSUPPORTED
+    assert pd(d=64) == pkv.PKV_ERR_UNSUPPORTED
+    assert pd(params=b.PlanParams(16, 32, 4, 16, 64, 512)) == pkv.PKV_ERR_INVALID_ARG   # Hkv mismatch
+    assert pd(max_tasks=100) == pkv.PKV_ERR_WORKSPACE                                  # below the plan's bound
+    # the slot limit: 8034 slots of 2080 B fit in 16 MiB - 64 KiB, 8035 do not
+    p1 = b.PlanParams(16, 32, 8, 1, 1, 512)
+    assert pd(B=1, params=b.PlanParams(16, 32, 8, 1, 1004, 512), max_tasks=8035) == pkv.PKV_ERR_WORKSPACE
+    assert pd(B=1, params=p1, max_tasks=8035) == pkv.PKV_ERR_WORKSPACE
+    assert pd(B=1, hq=64, hkv=8, params=p1, max_tasks=4018) == pkv.PKV_ERR_WORKSPACE   # G = 8: 4160-B slots
+
+
 @pytest.mark.parametrize("policy", [0, 1])
 def test_host_planner_matches_oracle(policy):
     """pkv_plan_host (C++) against the oracle's ref_plan: bit-exact task lists and offsets."""
