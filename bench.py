@@ -257,24 +257,32 @@ def measure(runner, steps, warmup, flush_bufs):
                 marker_ms=marker_ms)
 
 
+def read_ceiling(pkv, torch, buf, sink, nbytes, reps=7):
+    """Streaming-read bandwidth (GB/s) of the first `nbytes` of the 1 GiB buffer, from the
+    read kernel's own execution interval (launch-stamped events), each read after a full
+    pass over the buffer so that the bytes read are not in the 256 MB last-level cache."""
+    Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    view = buf[:nbytes - nbytes % 16]
+    us = []
+    for _ in range(reps):
+        pkv.pkv_stream_read(buf, sink)
+        e0, e1 = Ev(), Ev()
+        pkv.pkv_stream_read(view, sink, events=(e0, e1))
+        torch.cuda.synchronize()
+        us.append(e0.elapsed_time(e1) * 1e3)
+    return view.numel() / float(np.median(us)) / 1e3
+
+
 def calibrate(pkv, torch, flush_bufs, reps=10, launches=200):
     """Device constants of the cost model, measured in this run: beta = streaming-read
-    bandwidth of a 1 GiB read (GB/s), lambda = device time per back-to-back launch of a
-    near-empty kernel (us), from events around `launches` 16-byte reads queued behind
-    a backlog of large reads."""
+    bandwidth of a 1 GiB read (GB/s, the read kernel's own execution interval), lambda =
+    device time per back-to-back launch of a near-empty kernel (us), from events around
+    `launches` 16-byte reads queued behind a backlog of large reads."""
     Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     buf, sink = flush_bufs if flush_bufs is not None else (
         torch.zeros(1 << 30, dtype=torch.uint8, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda"))
     pkv.pkv_stream_read(buf, sink)
-    ms = []
-    for _ in range(reps):
-        e0, e1 = Ev(), Ev()
-        e0.record()
-        pkv.pkv_stream_read(buf, sink)
-        e1.record()
-        torch.cuda.synchronize()
-        ms.append(e0.elapsed_time(e1))
-    beta = buf.numel() / (float(np.median(ms)) / 1e3) / 1e9
+    beta = read_ceiling(pkv, torch, buf, sink, buf.numel(), reps)
     # launch gap: queue enough 1 GiB reads ahead that the host has enqueued every
     # small launch before the device reaches them, so the interval is device time
     small = buf[:16]
@@ -295,6 +303,32 @@ def head_pairs(hq, hkv, target):
     tasks per resident workgroup (one workgroup per compute unit)."""
     from paper_2606_26666_amd import costmodel
     return costmodel.head_pairs(hq, hkv) and target >= 2 * costmodel.CUS
+
+
+def split_range(runner, lens):
+    """(fewest, most) splits of an active row at the step over `lens`: the planner's
+    per-row split counts for the workqueue routes, the launch's S for the rectangular
+    grid, the per-group S for the bucket routes."""
+    from paper_2606_26666_amd import costmodel
+    lens = np.asarray(lens, dtype=np.int64)
+    act = lens > 0
+    if not act.any():
+        return [0, 0]
+    if runner.route in ("one-launch", "plan+fused", "two-kernel"):
+        _, offs, _ = runner.pkv.pkv_plan_host(lens, runner.params, runner.w.max_pages_per_row, with_tasks=False)
+        ns = np.diff(offs)[act]
+    elif runner.route == "rect":
+        S = runner.rect_splits()
+        tiles = -(-lens[act] // runner.w.tile_tokens)
+        ns = np.minimum(tiles, S)
+    else:
+        groups = costmodel.bucket_groups(lens, runner.route == "exact-buckets")
+        ns = []
+        for rows in groups:
+            S = costmodel.rect_split_count(rows.size, runner.w.hkv, runner.params)
+            ns += [min(S, -(-int(lens[i]) // runner.w.tile_tokens)) for i in rows if lens[i] > 0]
+        ns = np.asarray(ns)
+    return [int(ns.min()), int(ns.max())]
 
 
 def summarize(runner, m):
@@ -319,9 +353,11 @@ def summarize(runner, m):
         "alg_bytes_last_step": float(alg[-1]),
         "kv_bytes_per_step": float(np.mean(kv)),
         "decode_gbs": achieved,
+        "decode_frac_of_peak": achieved / HBM_PEAK_GBS,
         "step_gbs": float(np.mean(alg)) / (float(np.mean(m["step_ms"])) / 1e3) / 1e9,
         "tasks_per_step": float(np.mean(m["ntasks"])),
         "task_target": int(w.target_tasks),
+        "splits_per_row": split_range(runner, m["lens"][-1]),
         "kv_heads_per_workgroup": 2 if runner.route == "one-launch" and head_pairs(w.hq, w.hkv, w.target_tasks)
                                   else 1,
         "launches_per_step": launches_per_step(runner),
@@ -424,10 +460,15 @@ CALIBRATION = os.path.join(ROOT, "paper_2606_26666_amd", "calibration_mi355x.jso
 # sensitivity sweep of the one-launch workqueue plus every other route on the ragged
 # B8 trace and on B1 (exact buckets are left out: their step time includes host launch
 # time whenever the host falls behind)
+# (workload, route, policy, task target) steps the cost model is fitted on: the split
+# sensitivity sweep of the one-launch workqueue on B1 and B8 bimodal, the one-launch
+# route on the other traces, and every route of the bench's routes tables at the task
+# target of the cost model's rule (0) (exact buckets are left out: their step time
+# includes host launch time whenever the host falls behind)
 CAL_RUNS = ([(w, "one-launch", 1, t) for w in ("b1", "b8_bimodal") for t in (128, 256, 512, 1024)]
-            + [(w, "one-launch", 1, 256) for w in ("b8_uniform", "b8_zipf", "b4_bimodal")]
-            + [("b8_bimodal", r, 1, 256) for r in ("plan+fused", "two-kernel")]
-            + [(w, r, 0, 256) for w in ("b8_bimodal", "b8_uniform", "b1") for r in ("rect", "coarse-buckets")])
+            + [(w, "one-launch", 1, 0) for w in ("b8_uniform", "b8_zipf", "b4_bimodal")]
+            + [(w, r, 1, 0) for w in ("b1", "b8_bimodal", "b8_uniform")
+               for r in ("plan+fused", "two-kernel", "rect", "coarse-buckets")])
 
 
 def dataclass_dict(x):
@@ -446,19 +487,21 @@ def fit_cost_model(args, flush_bufs, probe, out_path):
         sh = r.shape(m["lens"][-1])
         us = float(np.mean(m["step_ms"])) * 1e3
         samples.append((sh, us))
-        rows.append((wl, route, policy, target, sh, us))
+        rows.append((wl, route, policy, int(r.w.target_tasks), sh, us, [int(x) for x in m["lens"][-1]]))
         del r
     cal = costmodel.fit(samples, probe["beta_read_gbs"], probe["launch_gap_us"])
     cal.note += f"; written by: python bench.py --calibrate {os.path.relpath(out_path, ROOT)}"
     cal.save(out_path)
     table = [{"workload": wl, "route": route, "policy": pol, "target": t, "measured_us": us,
-              "model_us": costmodel.estimate_us(sh, cal), "wg_per_cu": sh.workgroups / 256.0}
-             for (wl, route, pol, t, sh, us) in rows]
+              "model_us": costmodel.estimate_us(sh, cal), "wg_per_cu": sh.workgroups / 256.0, "lens": lens}
+             for (wl, route, pol, t, sh, us, lens) in rows]
     return cal, table
 
 
-def cost_model_view(runner, measured_us):
-    """The committed calibration's estimate of every route for the runner's last step."""
+def cost_model_view(runner, measured_us, routes_measured=None):
+    """The committed calibration's estimate of every route for the runner's last step,
+    the route it would choose and, when every route was timed on this workload
+    (`routes_measured`: {route: us per step}), the measured fastest one."""
     from paper_2606_26666_amd import costmodel
     if not os.path.exists(CALIBRATION):
         return None
@@ -467,9 +510,15 @@ def cost_model_view(runner, measured_us):
     est = {r: costmodel.estimate_us(costmodel.route_shape(r, lens, runner.params, runner.w.hq, runner.w.head_dim,
                                                          runner.w.max_pages_per_row), cal)
            for r in costmodel.ROUTES}
-    return {"chosen": min(est, key=est.get), "estimate_us": est, "measured_us": measured_us,
-            "calibration": {"beta_gbs": cal.beta_gbs, "probe_beta_gbs": cal.probe_beta_gbs,
-                            "launch_us": cal.launch_us, "c_min": cal.c_min, "fixed_us": cal.fixed_us}}
+    out = {"chosen": min(est, key=est.get), "estimate_us": est, "measured_us": measured_us,
+           "calibration": {"beta_gbs": cal.beta_gbs, "probe_beta_gbs": cal.probe_beta_gbs,
+                           "launch_us": cal.launch_us, "c_min": cal.c_min, "fixed_us": cal.fixed_us,
+                           "route_fixed_us": cal.route_fixed_us}}
+    if routes_measured:
+        out["measured_fastest"] = min(routes_measured, key=routes_measured.get)
+        out["routes_measured_us"] = routes_measured
+        out["chosen_is_fastest"] = out["chosen"] == out["measured_fastest"]
+    return out
 
 
 def seed_spread(args, workloads, seeds, first, flush_bufs):
@@ -500,7 +549,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="b1")
-    ap.add_argument("--also", default="b8_bimodal", help="comma-separated extra workloads, or 'none'")
+    ap.add_argument("--also", default="b8_bimodal,b8_uniform,b8_zipf,b4_bimodal",
+                    help="comma-separated extra workloads, or 'none'")
     ap.add_argument("--seed", type=int, default=20260623)
     ap.add_argument("--seeds", default="20260624,20260625,20260626,20260627",
                     help="further held-out seeds: the main workload and each --also workload are also run "
@@ -516,7 +566,7 @@ def main():
                          "planner inside the decode launch; two-kernel: planner, split kernel, merge kernel; "
                          "rect: rectangular (B, Hkv, S) grid + merge kernel; "
                          "exact-buckets / coarse-buckets: host-grouped rows, a rectangular launch pair per group")
-    ap.add_argument("--routes-table", default="b8_bimodal",
+    ap.add_argument("--routes-table", default="b1,b8_bimodal,b8_uniform",
                     help="comma-separated workloads on which every route is also timed with its Tab. 4 counters "
                          "('none' to skip)")
     ap.add_argument("--no-flush", action="store_true", help="keep KV warm in the last-level cache")
@@ -559,29 +609,48 @@ def main():
                       policy=args.policy, hkv=args.hkv)
     m = measure(main_run, args.steps, args.warmup, flush_bufs)
     s = summarize(main_run, m)
-    extra = {args.workload: s, "calibration": cal,
-             "cost_model": cost_model_view(main_run, s["ms_per_step"] * 1e3)}
+    extra = {args.workload: s, "calibration": cal}
+    runs = {args.workload: main_run}
+
+    def with_ceiling(res):
+        """The streaming-read ceiling at the step's KV size, beside the kernel's rate."""
+        if flush_bufs is not None:
+            nbytes = min(int(res["kv_bytes_per_step"]), flush_bufs[0].numel())
+            res["read_ceiling_gbs"] = read_ceiling(pkv, torch, flush_bufs[0], flush_bufs[1], nbytes)
+            res["decode_frac_of_read_ceiling"] = res["decode_gbs"] / res["read_ceiling_gbs"]
+        return res
+
+    with_ceiling(s)
     oracle_also = {}
     also = [x for x in args.also.split(",") if x and x != "none" and x != args.workload]
     for name in also:
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy, hkv=args.hkv)
-        extra[name] = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
+        extra[name] = with_ceiling(summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs)))
         if name == "b8_bimodal" and not args.no_cpu_baseline:
             oracle_also[name] = oracle_step_tok_s(r)
-        del r
+        runs[name] = r
     seeds = [int(x) for x in args.seeds.split(",") if x and x != "none" and int(x) != args.seed]
     if seeds:
         extra["seeds"] = seed_spread(args, [args.workload] + also, seeds,
                                      {args.workload: s, **{n: extra[n] for n in also}}, flush_bufs)
+    tables = {}
     for wl in [x for x in args.routes_table.split(",") if x and x != "none"]:
         table = {}
         for route in ROUTES:
-            r = Runner(wl, args.seed, args.target_tasks, 50, route=route, policy=args.policy, hkv=args.hkv)
-            res = summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs))
-            table[route] = {k: res[k] for k in ("tok_s", "ms_per_step", "launches_per_step", "split_wg_per_cu",
-                                                "useful_kv_mib", "merge_mib", "merge_launches")}
+            r = Runner(wl, args.seed, args.target_tasks, 50 if wl != "b1" else 20, route=route, policy=args.policy,
+                       hkv=args.hkv)
+            res = summarize(r, measure(r, min(args.steps * 2, 50 if wl != "b1" else 20), args.warmup, flush_bufs))
+            table[route] = {k: res[k] for k in ("tok_s", "ms_per_step", "decode_ms", "launches_per_step",
+                                                "split_wg_per_cu", "splits_per_row", "useful_kv_mib", "merge_mib",
+                                                "merge_launches")}
             del r
         extra["routes_" + wl] = table
+        tables[wl] = {rt: v["ms_per_step"] * 1e3 for rt, v in table.items()}
+    # the cost model's route choice for every workload timed above, against the measured
+    # fastest route where every route was timed
+    for name, r in runs.items():
+        extra[name]["cost_model"] = cost_model_view(r, extra[name]["ms_per_step"] * 1e3, tables.get(name))
+    extra["cost_model"] = extra[args.workload]["cost_model"]
     traffic = read_traffic(args.workload) if args.hkv == 8 else None  # the summaries cover Hkv = 8
     line = {
         "metric": METRIC,
@@ -600,6 +669,12 @@ def main():
                    "kv_layout": "[num_pages,16,Hkv,d]", "accumulate": "f32",
                    "route": args.route,
                    "split_policy": ["batch split count", "tile quota"][args.policy],
+                   # the tile-quota policy does not use split_min; the split counts the
+                   # planner gave the active rows at the last timed step:
+                   **({"split_min": main_run.w.split_min} if args.policy == 0 else {}),
+                   "split_max": main_run.w.split_max,
+                   "splits_per_row": s["splits_per_row"],
+                   "task_target": s["task_target"],
                    "llc_flushed": not args.no_flush, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": s["decode_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": s["decode_gbs"] / HBM_PEAK_GBS, "traffic": traffic,

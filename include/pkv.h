@@ -293,6 +293,11 @@ int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream
  * is written only if the data hashes to a fixed value. */
 int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream);
 
+/* pkv_stream_read with start/stop events stamped by the launch itself (the kernel's
+ * execution interval, as for pkv_decode_timed); either event may be NULL. */
+int pkv_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream,
+                          hipEvent_t start, hipEvent_t stop);
+
 #ifdef __cplusplus
 }
 #endif

@@ -72,6 +72,7 @@ _SIGS = {
     "pkv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "pkv_stream_copy": (ctypes.c_int, [_P, _P, _SZ, _P]),
     "pkv_stream_read": (ctypes.c_int, [_P, _SZ, _P, _P]),
+    "pkv_stream_read_timed": (ctypes.c_int, [_P, _SZ, _P, _P, _P, _P]),
 }
 
 
@@ -303,12 +304,17 @@ def pkv_stream_copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
     _check("pkv_stream_copy", lib().pkv_stream_copy(src.data_ptr(), dst.data_ptr(), n - n % 16, _stream(stream)))
 
 
-def pkv_stream_read(src: torch.Tensor, sink: torch.Tensor, stream=None):
+def pkv_stream_read(src: torch.Tensor, sink: torch.Tensor, stream=None, events=None):
+    """Streaming read of `src`; events: optional (start, stop) stamped with the kernel's
+    execution interval (pkv_stream_read_timed)."""
     if not (src.is_cuda and src.is_contiguous()):
         raise TypeError("pkv_stream_read needs a contiguous device tensor")
     n = src.numel() * src.element_size()
-    _check("pkv_stream_read", lib().pkv_stream_read(src.data_ptr(), n - n % 16, _dev(sink, torch.int32, "sink"),
-                                                    _stream(stream)))
+    args = (src.data_ptr(), n - n % 16, _dev(sink, torch.int32, "sink"), _stream(stream))
+    if events is None:
+        _check("pkv_stream_read", lib().pkv_stream_read(*args))
+    else:
+        _check("pkv_stream_read_timed", lib().pkv_stream_read_timed(*args, *_events(events)))
 
 
 class DecodeBuffers:

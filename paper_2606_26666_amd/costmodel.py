@@ -2,18 +2,26 @@
 
 For one decode step over lengths N_i, route r is priced as
 
-    T_r = sum_j KV_j / beta * max(1, C_min / C_j) + L_r * lambda + Merge_r / beta + T_0
+    T_r = sum_j KV_j / beta * max(1, C_min / C_j) * (1 - gamma [pairs])
+          + L_r * lambda + Merge_r / beta + T_0 + T_f(r)
 
 where the sum runs over the route's split launches j (one for the workqueue routes and
 the rectangular grid, one per group for the length buckets), KV_j is the K/V bytes launch
 j streams, C_j its split workgroups per compute unit, L_r the launches per step, Merge_r
 the partial-state bytes written and read back, beta the streaming-read bandwidth and
-lambda the device time per launch. The first three terms are the paper's model. T_0 is
-added here: on MI355X every step also pays a fixed chain of memory round trips (lengths,
-page ids, first pages, state store, completion counter, merge) of roughly 10 us that no
-term of the paper's model captures. lambda is measured by a probe; C_min, T_0 and the
-effective beta (the KV stream of a step runs below the probe's streaming-read rate, which
-is kept beside it) are fitted to measured steps (`fit`).
+lambda the device time per launch. The first three terms are the paper's model. Added
+here, because on MI355X they are not small against a step:
+  T_0     a fixed chain of memory round trips every step pays (lengths, page ids, first
+          pages, state store, completion counter, merge), roughly 10 us;
+  T_f(r)  a fixed term per route family (`FAMILY`: the one-launch route, whose planner
+          runs inside the launch; the routes behind a planner kernel; the rectangular
+          grids, which plan nothing), relative to the one-launch route;
+  gamma   the faster KV stream of the one-launch route when it runs KV-head pairs (each
+          workgroup then reads two heads' slices of every token, which evens out the
+          per-head and per-XCD read rates).
+lambda is measured by a probe; C_min, T_0, T_f, gamma and the effective beta (the KV
+stream of a step runs below the probe's streaming-read rate, which is kept beside it) are
+fitted to measured steps (`fit`).
 
 Everything here is host arithmetic over the planner's counts (`pkv_plan_host`); it
 launches nothing.
@@ -29,6 +37,9 @@ import numpy as np
 from . import _binding as _b
 
 ROUTES = ("one-launch", "plan+fused", "two-kernel", "rect", "exact-buckets", "coarse-buckets")
+# route families that share a fixed per-step term T_f
+FAMILY = {"one-launch": "one-launch", "plan+fused": "planner kernel", "two-kernel": "planner kernel",
+          "rect": "rectangular", "exact-buckets": "rectangular", "coarse-buckets": "rectangular"}
 CUS = 256                 # compute units of an MI355X
 SPLITS_PER_ROW_HEAD = 4   # splits per KV head per active row the task target leaves room for
 LAUNCHES = {"one-launch": 1, "plan+fused": 2, "two-kernel": 3}
@@ -44,6 +55,8 @@ class Calibration:
     fixed_us: float = 0.0    # per-step fixed latency T_0, us
     cus: int = 256           # compute units
     probe_beta_gbs: float = 0.0  # streaming-read bandwidth of the probe (a 1 GiB read), GB/s
+    route_fixed_us: dict = dataclasses.field(default_factory=dict)  # T_f per FAMILY entry, us
+    pair_gain: float = 0.0   # gamma: fraction of KV streaming time KV-head pairs save
     note: str = ""
 
     def save(self, path: str) -> None:
@@ -67,6 +80,8 @@ class RouteShape:
     launch_count: int
     merge_bytes: int
     merge_launches: int
+    route: str = "one-launch"
+    pairs: bool = False       # the one-launch route runs KV-head pairs
 
     @property
     def workgroups(self) -> int:
@@ -147,11 +162,12 @@ def route_shape(route: str, lens, params, hq: int = 32, d: int = 128,
     if route in LAUNCHES:
         maxp = max_pages_per_row or int(lens.max(initial=0)) // 16 + 1
         _, _, n = _b.pkv_plan_host(lens, params, maxp, with_tasks=False)
-        return RouteShape([(kv, n)], LAUNCHES[route], 2 * n * sb, 1 if route == "two-kernel" else 0)
+        pairs = route == "one-launch" and head_pairs(hq, hkv) and params.target_tasks >= 2 * CUS
+        return RouteShape([(kv, n)], LAUNCHES[route], 2 * n * sb, 1 if route == "two-kernel" else 0, route, pairs)
     if route == "rect":
         active = int(np.count_nonzero(lens))
         slots = lens.size * hkv * rect_split_count(active, hkv, params)
-        return RouteShape([(kv, slots)], 2, 2 * slots * sb, 1)
+        return RouteShape([(kv, slots)], 2, 2 * slots * sb, 1, route)
     if route in ("exact-buckets", "coarse-buckets"):
         launches, slots = [], 0
         groups = bucket_groups(lens, route == "exact-buckets")
@@ -159,7 +175,7 @@ def route_shape(route: str, lens, params, hq: int = 32, d: int = 128,
             s = rows.size * hkv * rect_split_count(rows.size, hkv, params)
             launches.append((int(lens[rows].sum()) * kv_tok, s))
             slots += s
-        return RouteShape(launches, 2 * len(groups), 2 * slots * sb, len(groups))
+        return RouteShape(launches, 2 * len(groups), 2 * slots * sb, len(groups), route)
     raise ValueError(f"unknown route {route}")
 
 
@@ -170,7 +186,10 @@ def estimate_us(shape: RouteShape, cal: Calibration) -> float:
     for kv, wgs in shape.launches:
         c = wgs / cal.cus
         t += kv / bw * max(1.0, cal.c_min / c) if c > 0 else 0.0
-    return t + shape.launch_count * cal.launch_us + shape.merge_bytes / bw + cal.fixed_us
+    if shape.pairs:
+        t *= 1.0 - cal.pair_gain
+    return (t + shape.launch_count * cal.launch_us + shape.merge_bytes / bw + cal.fixed_us
+            + cal.route_fixed_us.get(FAMILY[shape.route], 0.0))
 
 
 def choose_route(lens, params, cal: Calibration, routes=ROUTES, **kw):
@@ -180,29 +199,52 @@ def choose_route(lens, params, cal: Calibration, routes=ROUTES, **kw):
 
 
 def fit(samples, probe_beta_gbs: float, launch_us: float, cus: int = 256,
-        c_grid=None, beta_scales=None) -> Calibration:
-    """Fit C_min, T_0 and the effective beta to measured steps, lambda fixed by its probe.
+        c_grid=None, beta_scales=None, gamma_grid=None) -> Calibration:
+    """Fit the effective beta, C_min, gamma, T_0 and the per-family T_f to measured
+    steps, lambda fixed by its probe.
 
-    samples: [(RouteShape, measured_us)]. On a grid of (beta, C_min) the best T_0 is the
-    mean residual (least squares in T_0); the pair with the smallest squared error wins.
-    beta is searched as a fraction of the probe's streaming-read bandwidth.
+    samples: [(RouteShape, measured_us)]. On a grid of (beta, C_min, gamma) the best
+    intercepts are the mean residual of each route family (least squares in T_0 + T_f);
+    the grid point with the smallest squared error wins. T_0 is the one-launch family's
+    intercept (or the first family's, without one-launch samples) and T_f the other
+    families' offsets from it. beta is searched as a fraction of the probe's
+    streaming-read bandwidth.
     """
     if not samples:
         raise ValueError("no samples")
     if c_grid is None:
-        c_grid = np.round(np.arange(0.05, 8.0001, 0.05), 4)
+        c_grid = np.round(np.arange(0.1, 4.0001, 0.1), 4)
     if beta_scales is None:
         beta_scales = np.round(np.arange(0.60, 1.1001, 0.01), 4)
+    if gamma_grid is None:
+        gamma_grid = np.round(np.arange(0.0, 0.2001, 0.01), 4)
+    fams = [FAMILY[sh.route] for sh, _ in samples]
+    names = sorted(set(fams), key=lambda f: (f != "one-launch", f))
+    meas = np.array([m for _, m in samples], dtype=np.float64)
+    # per sample: KV bytes and workgroups per CU of each split launch, the fixed bytes and launches
+    lsum = np.array([sh.launch_count * launch_us for sh, _ in samples])
+    merge = np.array([sh.merge_bytes for sh, _ in samples], dtype=np.float64)
+    pairs = np.array([sh.pairs for sh, _ in samples])
     best = None
-    for bs in beta_scales:
-        for c in c_grid:
-            base = Calibration(probe_beta_gbs * float(bs), launch_us, float(c), 0.0, cus)
-            resid = np.array([m - estimate_us(sh, base) for sh, m in samples])
-            t0 = float(resid.mean())
-            err = float(((resid - t0) ** 2).sum())
-            if best is None or err < best[0] - 1e-9:
-                best = (err, float(bs), float(c), t0)
-    err, bs, c, t0 = best
+    for c in c_grid:
+        # KV bytes weighted by the occupancy factor, per sample
+        kvw = np.array([sum(kv * max(1.0, c / (w / cus)) for kv, w in sh.launches if w > 0) for sh, _ in samples])
+        for g in gamma_grid:
+            kvg = np.where(pairs, kvw * (1.0 - g), kvw)
+            for bs in beta_scales:
+                bw = probe_beta_gbs * float(bs) * 1e3
+                resid = meas - (kvg / bw + lsum + merge / bw)
+                err = 0.0
+                icpt = {}
+                for f in names:
+                    sel = np.array([x == f for x in fams])
+                    icpt[f] = float(resid[sel].mean())
+                    err += float(((resid[sel] - icpt[f]) ** 2).sum())
+                if best is None or err < best[0] - 1e-9:
+                    best = (err, float(bs), float(c), float(g), icpt)
+    err, bs, c, g, icpt = best
+    t0 = icpt[names[0]]
     rms = math.sqrt(err / len(samples))
     return Calibration(probe_beta_gbs * bs, launch_us, c, t0, cus, probe_beta_gbs,
+                       route_fixed_us={f: icpt[f] - t0 for f in names}, pair_gain=g,
                        note=f"fit over {len(samples)} steps, rms {rms:.2f} us")

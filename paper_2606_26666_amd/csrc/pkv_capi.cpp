@@ -320,8 +320,13 @@ int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream
 }
 
 int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream) {
+  return pkv_stream_read_timed(src, bytes, sink, stream, nullptr, nullptr);
+}
+
+int pkv_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream, hipEvent_t start,
+                          hipEvent_t stop) {
   if (!src || !sink || bytes % 16 != 0 || !aligned(src, 16) || !aligned(sink, 4)) return PKV_ERR_INVALID_ARG;
-  return from_hip(launch_read(src, bytes, sink, stream));
+  return from_hip(launch_read(src, bytes, sink, stream, start, stop));
 }
 
 }  // extern "C"

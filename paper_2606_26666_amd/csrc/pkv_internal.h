@@ -85,6 +85,7 @@ hipError_t launch_ws_init(void* ws, size_t bytes, uint32_t counters, hipStream_t
 // device zeroes its counters on stream s
 hipError_t static_scratch(hipStream_t s, char** base);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
-hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s);
+hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s, hipEvent_t start = nullptr,
+                       hipEvent_t stop = nullptr);
 
 }  // namespace pkv

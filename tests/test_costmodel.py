@@ -55,21 +55,45 @@ def test_choose_route_prefers_fewer_launches_at_equal_work():
 
 
 def test_fit_recovers_planted_constants():
-    truth = cm.Calibration(beta_gbs=5400.0, launch_us=1.5, c_min=1.35, fixed_us=9.0)
+    truth = cm.Calibration(beta_gbs=5400.0, launch_us=1.5, c_min=1.3, fixed_us=9.0,
+                           route_fixed_us={"one-launch": 0.0, "planner kernel": 1.25, "rectangular": -2.0},
+                           pair_gain=0.06)
     r = np.random.Generator(np.random.PCG64(3))
     samples = []
     for target in (64, 128, 256, 512, 1024):
         for lens in ([32769], list(r.integers(1000, 32768, size=8))):
-            for route in ("one-launch", "rect", "coarse-buckets"):
+            for route in ("one-launch", "plan+fused", "rect", "coarse-buckets"):
                 sh = cm.route_shape(route, lens, params(target=target, policy=1 if route == "one-launch" else 0))
                 samples.append((sh, cm.estimate_us(sh, truth)))
+    assert any(sh.pairs for sh, _ in samples) and not all(sh.pairs for sh, _ in samples)
     got = cm.fit(samples, 6000.0, truth.launch_us)          # probe 6000, true effective 0.9 of it
-    assert got.beta_gbs == pytest.approx(5400.0) and got.c_min == pytest.approx(1.35)
+    assert got.beta_gbs == pytest.approx(5400.0) and got.c_min == pytest.approx(1.3)
+    assert got.pair_gain == pytest.approx(0.06)
     assert got.fixed_us == pytest.approx(9.0, abs=1e-6) and got.probe_beta_gbs == 6000.0
+    for fam, v in truth.route_fixed_us.items():
+        assert got.route_fixed_us[fam] == pytest.approx(v, abs=1e-6)
+
+
+def test_route_terms_in_the_estimate():
+    """A family's fixed term is added to every route of that family; the pair gain scales
+    only the KV streaming time of a one-launch step that runs KV-head pairs."""
+    base = cm.Calibration(beta_gbs=5000.0, launch_us=2.0, c_min=1.0, fixed_us=7.0)
+    more = cm.Calibration(beta_gbs=5000.0, launch_us=2.0, c_min=1.0, fixed_us=7.0,
+                          route_fixed_us={"rectangular": 3.0}, pair_gain=0.1)
+    lens = [20000] * 8
+    for route in cm.ROUTES:
+        sh = cm.route_shape(route, lens, params(target=512, policy=1))
+        d = cm.estimate_us(sh, more) - cm.estimate_us(sh, base)
+        if cm.FAMILY[route] == "rectangular":
+            assert d == pytest.approx(3.0)
+        elif sh.pairs:
+            assert route == "one-launch" and d == pytest.approx(-0.1 * 8 * 20000 * 4096 / 5e6)
+        else:
+            assert d == pytest.approx(0.0)
 
 
 def test_calibration_roundtrip(tmp_path):
-    cal = cm.Calibration(5500.0, 1.54, 1.25, 10.5, 256, 6087.7, note="x")
+    cal = cm.Calibration(5500.0, 1.54, 1.25, 10.5, 256, 6087.7, {"rectangular": -1.0}, 0.04, note="x")
     path = tmp_path / "cal.json"
     cal.save(str(path))
     assert cm.Calibration.load(str(path)) == cal

@@ -109,8 +109,7 @@ class Workload:
                 "head_dim": self.head_dim, "page_size": self.page_size,
                 "prompt_lens": [int(x) for x in self.seq_lens], "append": self.append, "steps": self.steps,
                 "num_pages": self.num_pages, "rho": self.rho, "seed": self.seed,
-                "split_bounds": [self.split_min, self.split_max],
-                "target_tasks": self.target_tasks, "tile_tokens": self.tile_tokens}
+                "tile_tokens": self.tile_tokens}
 
 
 def _build(name, lens, steps, rho, seed, rng_pages, num_pages=None, split=(16, 64),
