@@ -13,7 +13,8 @@ import re
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libpkv.so")
+# PKV_LIBRARY selects another build of the same sources (an A/B build for measurement)
+LIB_PATH = os.environ.get("PKV_LIBRARY") or os.path.join(HERE, "libpkv.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "pkv.h")
 
 PKV_OK = 0

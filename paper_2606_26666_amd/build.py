@@ -24,9 +24,12 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False, extra_flags: list[str] | None = None) -> str:
-    """Compile every source and link libpkv.so next to this file. Always recompiles."""
-    tmp = LIB + ".tmp"
+def build(verbose: bool = False, extra_flags: list[str] | None = None, out: str | None = None) -> str:
+    """Compile every source and link libpkv.so next to this file (or at `out`: an A/B
+    build with `extra_flags`, loaded through the PKV_LIBRARY environment variable).
+    Always recompiles."""
+    lib = out or LIB
+    tmp = lib + ".tmp"
     cmd = [hipcc(), *HIP_FLAGS, *(extra_flags or []), "-shared", "-o", tmp,
            *[os.path.join(CSRC, s) for s in SOURCES]]
     res = subprocess.run(cmd, cwd=CSRC, capture_output=True, text=True)
@@ -34,9 +37,14 @@ def build(verbose: bool = False, extra_flags: list[str] | None = None) -> str:
         raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + res.stdout + res.stderr)
     if verbose:
         print(" ".join(cmd))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose=True, extra_flags=sys.argv[1:]))
+    # python build.py [--out PATH] [hipcc flags...]
+    argv = sys.argv[1:]
+    out = None
+    if argv[:1] == ["--out"]:
+        out, argv = os.path.abspath(argv[1]), argv[2:]
+    print(build(verbose=True, extra_flags=argv, out=out))

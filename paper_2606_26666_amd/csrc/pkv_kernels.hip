@@ -693,9 +693,16 @@ typedef _Float16 h4v __attribute__((ext_vector_type(4)));
 typedef short s4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s4v lds_s4v;
 
+// The matrix-core body runs G > PKV_VALU_BODY_MAX_G (default: G = 4 and 8). A library
+// built with -DPKV_VALU_BODY_MAX_G=4 (or 8) runs the VALU body up to that G instead: an
+// A/B build whose instruction and busy counters are set against the default build's to
+// back the choice of body. Results agree with the oracle either way.
+#ifndef PKV_VALU_BODY_MAX_G
+#define PKV_VALU_BODY_MAX_G 2
+#endif
 template <int G>
 constexpr bool mfma_task() {
-  return G == 4 || G == 8;
+  return G > PKV_VALU_BODY_MAX_G;
 }
 
 // The phases and covers() are those of ValuTask. NH = 2 runs KV heads g and g + 1 of
@@ -1622,7 +1629,7 @@ hipError_t launch_decode_g(const DecodeArgs& a, int mode, int grid, hipStream_t 
     // KV-head pairs when the task target gives every resident workgroup two tasks (G = 4:
     // at G = 8 the pair merge needs two rounds of loads and the pairs ran 11% slower on
     // the B8 traces)
-    if constexpr (G == 4) {
+    if constexpr (G == 4 && mfma_task<G>()) {  // the VALU body runs one KV head
       static const int resident2 = resident_blocks((const void*)split_kernel<G, W, true, true, 2>, W * 64);
       if (a.Hkv % 2 == 0 && a.plan.target_tasks >= 2 * resident2) {
         const int pairs = grid / 2;
