@@ -87,9 +87,10 @@ __device__ __forceinline__ void unpack8(const uint4& u, float f[8]) {
 constexpr float kNegInf = -__builtin_inff();
 
 // ---------------------------------------------------------------------------------
-// Partial-state slots (one per task): fp32 acc[G][D], then m[G] and l[G], padded to a
-// multiple of 16 bytes. m is in log2 units: scores are scaled by sm_scale*log2(e) and
-// exponentiated with exp2. l < 0 marks a split that met an invalid page.
+// Partial-state slots (one per task): fp32 acc[G][D], then (m, l) of each of the G heads
+// side by side (one 8-byte load fetches both), padded to a multiple of 16 bytes. m is in
+// log2 units: scores are scaled by sm_scale*log2(e) and exponentiated with exp2. l < 0
+// marks a split that met an invalid page.
 template <int G> constexpr int slot_floats() { return G * D + ((2 * G + 3) / 4) * 4; }
 
 // Split s of a row with `tiles` tiles cut into ns splits starts at tile
@@ -107,6 +108,7 @@ __device__ __forceinline__ int split_bound(int s, int tiles, int ns) {
 constexpr int kSc1 = 16;  // cache-policy operand of a buffer access: sc1
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t slots_rsrc(const DecodeArgs& a, int slot_bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(a.partials, (short)0, a.max_tasks * slot_bytes, 0x00020000);
@@ -115,6 +117,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t slots_rsrc(const DecodeArgs& a
 template <bool COHERENT>
 __device__ __forceinline__ float ld_state(__amdgpu_buffer_rsrc_t r, int off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, COHERENT ? kSc1 : 0));
+}
+template <bool COHERENT>
+__device__ __forceinline__ v2f ld_state2(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(v2f, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, COHERENT ? kSc1 : 0));
 }
 template <bool COHERENT>
 __device__ __forceinline__ v4f ld_state4(__amdgpu_buffer_rsrc_t r, int off) {
@@ -191,33 +197,51 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
   // At most four runs (32 splits): the four lanes of each DPP quad hold runs 0-3 of the
   // same CPT float4 columns (lane r: run r, i.e. splits 8r..8r+7), so the maximum, the
   // marker and the run sums are exchanged inside the quad, with no LDS and no barrier.
-  // Each thread issues all of its loads (8 m, 8 l, 8 CPT acc float4) at once. The
-  // operations and their order are those of the general path below.
+  // A wave's 16 CPT columns lie in at most two query heads (one for CPT <= 2); lane j of
+  // the wave loads (m, l) of split j % 32 of the wave's head j / 32 in one 8-byte load,
+  // and each lane takes those of its run's eight splits by lane shuffles. Per wave that
+  // is 1 + 8 CPT vector loads, all in flight together. The operations and their order
+  // are those of the general path below.
   if (nsplit <= 4 * kMergeRun) {
-    constexpr int CPT = 4 * E4 >= NT ? 4 * E4 / NT : 1;  // float4 columns per thread
-    static_assert(CPT <= 4 && (D / 4) % CPT == 0, "a thread's columns lie in one query head");
+    constexpr int CPT = 4 * E4 > NT ? 4 * E4 / NT : 1;  // float4 columns per thread
+    constexpr int HPW = CPT > 2 ? CPT / 2 : 1;          // query heads per wave
+    static_assert(CPT <= 4 && 4 * E4 <= CPT * NT && HPW * 32 <= 64, "quad merge shape");
     const int r = lane & 3;
     const int e40 = (tid >> 2) * CPT;  // this quad's first float4 column
     const bool active = e40 < E4;
     const int e4a = active ? e40 : 0;
-    const int hh = e4a / E4H;                // KV head within the NH merged
-    const int hl = ((e4a - hh * E4H) * 4) / D;  // query head within KV head hh
-    float mq[kMergeRun], lq[kMergeRun];
+    const int hh = e4a / E4H;                   // KV head within the NH merged
+    // (m, l) of split lane % 32 of the wave's query head lane / 32
+    const int wave_e4 = wave * 16 * CPT;        // the wave's first float4 column
+    const int jh = lane >> 5, js = lane & 31;
+    const int e4j = wave_e4 + jh * (D / 4);     // first column of that query head
+    int ml_off = kOutOfRange;
+    if (jh < HPW && e4j < E4 && js < nsplit) {
+      const int hhj = e4j / E4H;
+      ml_off = soff(js, hhj) + (G * D + 2 * (((e4j - hhj * E4H) * 4) / D)) * 4;
+    }
+    const v2f ml = ld_state2<COHERENT>(pr, ml_off);
     v4f vq[CPT][kMergeRun];
 #pragma unroll
     for (int u = 0; u < kMergeRun; ++u) {  // a state that does not exist reads as zero
       const int sidx = r * kMergeRun + u;
       const int off = sidx < nsplit ? soff(sidx, hh) : kOutOfRange;
-      mq[u] = ld_state<COHERENT>(pr, off + (G * D + hl) * 4);
-      lq[u] = ld_state<COHERENT>(pr, off + (G * D + G + hl) * 4);
 #pragma unroll
       for (int c = 0; c < CPT; ++c) vq[c][u] = ld_state4<COHERENT>(pr, off + (e4a - hh * E4H + c) * 16);
+    }
+    const int src0 = (HPW > 1 ? ((e4a - wave_e4) * 4 / D) * 32 : 0) + r * kMergeRun;  // lane of the run's first split
+    float mq[kMergeRun], lq[kMergeRun];
+#pragma unroll
+    for (int u = 0; u < kMergeRun; ++u) {
+      mq[u] = __shfl(ml.x, src0 + u);
+      lq[u] = __shfl(ml.y, src0 + u);
     }
     float M = kNegInf, bd = 0.0f;
 #pragma unroll
     for (int u = 0; u < kMergeRun; ++u) {
-      M = fmaxf(M, r * kMergeRun + u < nsplit ? mq[u] : kNegInf);
-      bd = fmaxf(bd, lq[u] < 0.0f ? 1.0f : 0.0f);
+      const bool ok = r * kMergeRun + u < nsplit;
+      M = fmaxf(M, ok ? mq[u] : kNegInf);
+      bd = fmaxf(bd, ok && lq[u] < 0.0f ? 1.0f : 0.0f);
     }
     M = fmaxf(M, dpp<0xB1>(M));  // quad_perm [1,0,3,2]
     M = fmaxf(M, dpp<0x4E>(M));  // quad_perm [2,3,0,1]
@@ -272,10 +296,10 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     for (int k = 0; k < KPT; ++k) {
       const int e = tid + k * NT;
       const bool ok = e < cnt * GH;
-      const int off = ok ? soff(s0 + e / GH, my_hh) + (G * D + my_h) * 4 : kOutOfRange;
-      const float m = ld_state<COHERENT>(pr, off);
-      lv[k] = ld_state<COHERENT>(pr, off + G * 4);  // l sits G floats after m (0 when absent)
-      mv[k] = ok ? m : kNegInf;
+      const int off = ok ? soff(s0 + e / GH, my_hh) + (G * D + 2 * my_h) * 4 : kOutOfRange;
+      const v2f ml = ld_state2<COHERENT>(pr, off);  // (m, l); zeros when absent
+      lv[k] = ml.y;
+      mv[k] = ok ? ml.x : kNegInf;
     }
   };
   // max and marker over this thread's states, then over lanes of the same head, then
@@ -453,8 +477,8 @@ __device__ __forceinline__ void finish_task(const DecodeArgs& a, int slot, float
     }
     st_state4<COHERENT>(pr, so + e4 * 16, A);
     if ((e4 * 4) % D == 0) {
-      st_state<COHERENT>(pr, so + (G * D + h) * 4, M);
-      st_state<COHERENT>(pr, so + (G * D + G + h) * 4, any_bad ? -1.0f : L);
+      st_state<COHERENT>(pr, so + (G * D + 2 * h) * 4, M);
+      st_state<COHERENT>(pr, so + (G * D + 2 * h + 1) * 4, any_bad ? -1.0f : L);
     }
   }
 }
@@ -956,7 +980,7 @@ __device__ __forceinline__ void write_neutral(const DecodeArgs& a, int slot) {
   constexpr int SF = slot_floats<G>();
   const __amdgpu_buffer_rsrc_t pr = slots_rsrc(a, SF * 4);
   for (int e = threadIdx.x; e < SF; e += blockDim.x)
-    st_state<false>(pr, (slot * SF + e) * 4, (e >= G * D && e < G * D + G) ? kNegInf : 0.0f);
+    st_state<false>(pr, (slot * SF + e) * 4, (e >= G * D && e < G * D + 2 * G && (e - G * D) % 2 == 0) ? kNegInf : 0.0f);
 }
 
 template <int G>
