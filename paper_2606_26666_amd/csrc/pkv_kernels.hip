@@ -278,12 +278,13 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     };
     const float L = ordered(lacc);
     const bool zero = M == kNegInf || bd != 0.0f;
+    const float iL = 1.0f / L;  // one division per head, then products
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       const float o0 = ordered(acc[c].x), o1 = ordered(acc[c].y), o2 = ordered(acc[c].z), o3 = ordered(acc[c].w);
       if (active && r == 0) {
-        const unsigned lo = f32_to_f16_bits(zero ? 0.0f : o0 / L) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o1 / L) << 16);
-        const unsigned hi = f32_to_f16_bits(zero ? 0.0f : o2 / L) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o3 / L) << 16);
+        const unsigned lo = f32_to_f16_bits(zero ? 0.0f : o0 * iL) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o1 * iL) << 16);
+        const unsigned hi = f32_to_f16_bits(zero ? 0.0f : o2 * iL) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o3 * iL) << 16);
         *reinterpret_cast<uint2*>(out_grp + (e40 + c) * 4) = make_uint2(lo, hi);
       }
     }
@@ -425,7 +426,7 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     const int e = tid + q * NT;
     if (e >= GH * D) break;
     const int h = e / D;
-    const float o = (sM[h] == kNegInf || sBad[h] != 0.0f) ? 0.0f : A[q] / sL[h];
+    const float o = (sM[h] == kNegInf || sBad[h] != 0.0f) ? 0.0f : A[q] * (1.0f / sL[h]);
     out_grp[e] = f32_to_f16_bits(o);
   }
 }
