@@ -273,6 +273,27 @@ def read_ceiling(pkv, torch, buf, sink, nbytes, reps=7):
     return view.numel() / float(np.median(us)) / 1e3
 
 
+def page_read_us(pkv, torch, runner, flush_bufs, reps=7):
+    """Read time (us) of the decode's pages in the decode's pattern: the library's
+    read-only probe (pkv_stream_read_pages) over the last step's task list, with the
+    decode's KV heads per workgroup, each run after the cache-evicting read; median of
+    the runs' launch-stamped execution intervals. None for routes without a task list."""
+    if runner.route not in ("one-launch", "plan+fused", "two-kernel") or flush_bufs is None:
+        return None
+    Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    w = runner.w
+    hpw = 2 if runner.route == "one-launch" and head_pairs(w.hq, w.hkv, w.target_tasks) else 1
+    us = []
+    for _ in range(reps):
+        pkv.pkv_stream_read(flush_bufs[0], flush_bufs[1])
+        e0, e1 = Ev(), Ev()
+        pkv.pkv_stream_read_pages(runner.k, runner.v, runner.bt, runner.bufs.tasks, runner.bufs.num_tasks, hpw,
+                                  flush_bufs[1], events=(e0, e1))
+        torch.cuda.synchronize()
+        us.append(e0.elapsed_time(e1) * 1e3)
+    return float(np.median(us))
+
+
 def calibrate(pkv, torch, flush_bufs, reps=10, launches=200):
     """Device constants of the cost model, measured in this run: beta = streaming-read
     bandwidth of a 1 GiB read (GB/s, the read kernel's own execution interval), lambda =
@@ -612,20 +633,26 @@ def main():
     extra = {args.workload: s, "calibration": cal}
     runs = {args.workload: main_run}
 
-    def with_ceiling(res):
-        """The streaming-read ceiling at the step's KV size, beside the kernel's rate."""
+    def with_ceiling(res, runner):
+        """Two read ceilings beside the kernel's rate: a contiguous streaming read of the
+        step's KV size, and the read-only probe of the decode's own pages and pattern."""
         if flush_bufs is not None:
             nbytes = min(int(res["kv_bytes_per_step"]), flush_bufs[0].numel())
             res["read_ceiling_gbs"] = read_ceiling(pkv, torch, flush_bufs[0], flush_bufs[1], nbytes)
             res["decode_frac_of_read_ceiling"] = res["decode_gbs"] / res["read_ceiling_gbs"]
+            pr = page_read_us(pkv, torch, runner, flush_bufs)
+            if pr is not None:
+                res["page_read_us"] = pr
+                res["page_read_gbs"] = res["kv_bytes_per_step"] / pr / 1e3
+                res["decode_frac_of_page_read"] = pr / (res["decode_ms"] * 1e3)
         return res
 
-    with_ceiling(s)
+    with_ceiling(s, main_run)
     oracle_also = {}
     also = [x for x in args.also.split(",") if x and x != "none" and x != args.workload]
     for name in also:
         r = Runner(name, args.seed, args.target_tasks, 50, route=args.route, policy=args.policy, hkv=args.hkv)
-        extra[name] = with_ceiling(summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs)))
+        extra[name] = with_ceiling(summarize(r, measure(r, min(args.steps * 2, 50), args.warmup, flush_bufs)), r)
         if name == "b8_bimodal" and not args.no_cpu_baseline:
             oracle_also[name] = oracle_step_tok_s(r)
         runs[name] = r
@@ -680,6 +707,7 @@ def main():
                      "frac": s["decode_gbs"] / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "split_kernel" + (" (planner inside)" if args.route == "one-launch" else ""),
                      "alg_bytes_per_launch": s["alg_bytes_last_step"],
+                     "read_ceiling_gbs": s.get("read_ceiling_gbs"), "page_read_gbs": s.get("page_read_gbs"),
                      "kernel_source_sha256": kernel_hash()},
         "cpu_baseline": None if args.no_cpu_baseline else {
             **cpu_baseline(main_run, args.steps),

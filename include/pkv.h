@@ -298,6 +298,34 @@ int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s
 int pkv_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream,
                           hipEvent_t start, hipEvent_t stop);
 
+/* Read-only probe of the decode kernel's KV access pattern (the read-bandwidth term of
+ * the cost model, Sec. 3.5, measured for the paged layout of Sec. 3.2 instead of a
+ * contiguous stream). For each of the first min(*num_tasks, max_tasks) records of
+ * `tasks` (as pkv_plan / pkv_plan_decode write them), the K and V bytes of the task's
+ * KV heads over the pages of its token range are read with the loads, waves, loads in
+ * flight, grid and task-to-workgroup mapping of the one-launch decode kernel:
+ * heads_per_workgroup = 1 runs one task per workgroup, 2 the tasks 2p and 2p + 1 (KV
+ * heads g, g + 1) together, as the decode's KV-head pairs do. No query is read, nothing
+ * is computed or written except `sink`, a device word written only if the data hash to
+ * a fixed value. Its duration is the time to read the decode's pages in the decode's
+ * pattern: the read ceiling of a decode step with that plan.
+ *   k_cache, v_cache  device, [num_pages, 16, Hkv, d] fp16 (16-byte aligned)
+ *   block_table       device int32 [B, max_pages_per_row]
+ *   tasks, num_tasks  device, a plan's task list and count; records naming a row, head
+ *                     or token range outside the arguments' bounds are skipped, and
+ *                     page ids outside [0, num_pages) are not read
+ *   d                 must be 128 (PKV_ERR_UNSUPPORTED otherwise)
+ *   start, stop       events stamped by the launch itself (kernel execution interval);
+ *                     either may be NULL
+ * Returns PKV_ERR_INVALID_ARG for null or misaligned pointers, non-positive sizes,
+ * Hkv > 256, heads_per_workgroup not 1 or 2 or not dividing Hkv. Enqueues one kernel on
+ * `stream`; allocates nothing. */
+int pkv_stream_read_pages(const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                          const int32_t* block_table, int32_t max_pages_per_row, int32_t B, int32_t Hkv, int32_t d,
+                          const pkv_task* tasks, const int32_t* num_tasks, int32_t max_tasks,
+                          int32_t heads_per_workgroup, uint32_t* sink, hipStream_t stream, hipEvent_t start,
+                          hipEvent_t stop);
+
 #ifdef __cplusplus
 }
 #endif

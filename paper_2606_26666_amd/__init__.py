@@ -33,6 +33,7 @@ from ._binding import (  # noqa: F401
     pkv_plan_decode_noalloc,
     pkv_stream_copy,
     pkv_stream_read,
+    pkv_stream_read_pages,
     pkv_workspace_init,
     pkv_workspace_size,
 )

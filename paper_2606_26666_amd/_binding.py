@@ -74,6 +74,8 @@ _SIGS = {
     "pkv_stream_copy": (ctypes.c_int, [_P, _P, _SZ, _P]),
     "pkv_stream_read": (ctypes.c_int, [_P, _SZ, _P, _P]),
     "pkv_stream_read_timed": (ctypes.c_int, [_P, _SZ, _P, _P, _P, _P]),
+    "pkv_stream_read_pages": (ctypes.c_int, [_P, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _P, _I32, _I32, _P,
+                                             _P, _P, _P]),
 }
 
 
@@ -316,6 +318,22 @@ def pkv_stream_read(src: torch.Tensor, sink: torch.Tensor, stream=None, events=N
         _check("pkv_stream_read", lib().pkv_stream_read(*args))
     else:
         _check("pkv_stream_read_timed", lib().pkv_stream_read_timed(*args, *_events(events)))
+
+
+def pkv_stream_read_pages(k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,
+                          tasks: torch.Tensor, num_tasks: torch.Tensor, heads_per_workgroup: int,
+                          sink: torch.Tensor, stream=None, events=None):
+    """Read-only probe of the decode kernel's page pattern over a plan's task list
+    (k_cache, v_cache [num_pages, 16, Hkv, d] fp16; tasks [max_tasks, 5] int32);
+    events: optional (start, stop) stamped with the kernel's execution interval."""
+    num_pages, _, hkv, d = k_cache.shape
+    B, maxp = block_table.shape
+    ev = _events(events) or (None, None)
+    _check("pkv_stream_read_pages", lib().pkv_stream_read_pages(
+        _dev(k_cache, torch.float16, "k_cache"), _dev(v_cache, torch.float16, "v_cache"), num_pages,
+        _dev(block_table, torch.int32, "block_table"), maxp, B, hkv, d, _dev(tasks, torch.int32, "tasks"),
+        _dev(num_tasks, torch.int32, "num_tasks"), tasks.shape[0], heads_per_workgroup,
+        _dev(sink, torch.int32, "sink"), _stream(stream), *ev))
 
 
 class DecodeBuffers:

@@ -329,6 +329,26 @@ int pkv_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, hipStre
   return from_hip(launch_read(src, bytes, sink, stream, start, stop));
 }
 
+int pkv_stream_read_pages(const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
+                          const int32_t* block_table, int32_t max_pages_per_row, int32_t B, int32_t Hkv, int32_t d,
+                          const pkv_task* tasks, const int32_t* num_tasks, int32_t max_tasks,
+                          int32_t heads_per_workgroup, uint32_t* sink, hipStream_t stream, hipEvent_t start,
+                          hipEvent_t stop) {
+  if (!k_cache || !v_cache || !block_table || !tasks || !num_tasks || !sink) return PKV_ERR_INVALID_ARG;
+  if (num_pages < 1 || max_pages_per_row < 1 || B < 1 || Hkv < 1 || Hkv > 256 || max_tasks < 1)
+    return PKV_ERR_INVALID_ARG;
+  if ((int64_t)max_pages_per_row * kPageSize > INT32_MAX) return PKV_ERR_INVALID_ARG;
+  if (d != kHeadDim) return PKV_ERR_UNSUPPORTED;
+  if (heads_per_workgroup != 1 && heads_per_workgroup != 2) return PKV_ERR_INVALID_ARG;
+  if (Hkv % heads_per_workgroup != 0) return PKV_ERR_INVALID_ARG;
+  if (!aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(tasks, 4) || !aligned(num_tasks, 4) ||
+      !aligned(sink, 4))
+    return PKV_ERR_INVALID_ARG;
+  const PageReadArgs a{k_cache, v_cache, block_table, tasks, num_tasks, sink, num_pages, max_pages_per_row, B, Hkv,
+                       max_tasks};
+  return from_hip(launch_page_read(a, heads_per_workgroup, stream, start, stop));
+}
+
 }  // extern "C"
 
 namespace {

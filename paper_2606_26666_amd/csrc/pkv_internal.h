@@ -85,6 +85,18 @@ hipError_t launch_ws_init(void* ws, size_t bytes, uint32_t counters, hipStream_t
 // device zeroes its counters on stream s
 hipError_t static_scratch(hipStream_t s, char** base);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+// Arguments of the read-only probe of the decode's page pattern (pkv_stream_read_pages).
+struct PageReadArgs {
+  const uint16_t* k;
+  const uint16_t* v;
+  const int32_t* block_table;
+  const pkv_task* tasks;
+  const int32_t* num_tasks;
+  unsigned* sink;
+  int32_t num_pages, max_pages_per_row, B, Hkv, max_tasks;
+};
+hipError_t launch_page_read(const PageReadArgs& a, int heads_per_workgroup, hipStream_t s, hipEvent_t start,
+                            hipEvent_t stop);
 hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s, hipEvent_t start = nullptr,
                        hipEvent_t stop = nullptr);
 

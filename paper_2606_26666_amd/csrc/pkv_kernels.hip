@@ -1613,6 +1613,82 @@ __global__ __launch_bounds__(256) void read_kernel(const uint4* __restrict__ src
   if (x == 0x9E3779B9u) *sink = x;  // keeps the loads; practically never taken
 }
 
+// Read-only probe of the decode kernel's KV access pattern: for every task of a task
+// list (records as the planner writes them), the waves of a workgroup read the K and V
+// bytes of the task's NH KV heads over its pages as the decode body does (wave w takes
+// pages w, w + W, ... of the task, page ids fetched 64 at a time, per page and head four
+// 16-byte buffer loads of K in the matrix-core body's K layout and four of V; two
+// (page, head) units in flight per wave: two pages of one head, or one page of each of
+// two heads), with the decode's grid (one workgroup per compute unit, held by the LDS
+// reservation) and task-to-workgroup mapping. Nothing else: no queries, no arithmetic
+// beyond folding the bytes into a sink word, no state, no merge. Its time is the read
+// time of the decode's pages in the decode's pattern.
+constexpr int kPageReadHoldWords = 24 * 1024;  // 96 KiB of LDS: one workgroup per compute unit
+
+template <int W, int NH>
+__global__ __launch_bounds__(W * 64) void page_read_kernel(PageReadArgs a) {
+  __shared__ unsigned hold[kPageReadHoldWords];
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int grp = lane >> 4, col = lane & 15;
+  const size_t tok_stride = (size_t)a.Hkv * D;  // halves between consecutive tokens
+  const size_t page_stride = (size_t)P * tok_stride;
+  const int tok_b = (int)(tok_stride * 2);
+  const int page_bytes = (int)(page_stride * 2);
+  int ntasks = uniform(*a.num_tasks);
+  if (ntasks > a.max_tasks) ntasks = a.max_tasks;
+  unsigned x = 0;
+  for (int t = NH * blockIdx.x; t + NH <= ntasks; t += NH * gridDim.x) {
+    const int* tp = reinterpret_cast<const int*>(a.tasks + t);
+    const int row = uniform(tp[0]), g = uniform(tp[1]), t0 = uniform(tp[3]), t1 = uniform(tp[4]);
+    if (row < 0 || row >= a.B || g < 0 || g % NH != 0 || g + NH > a.Hkv || t0 < 0 || t1 <= t0 ||
+        t1 > a.max_pages_per_row * P)
+      continue;  // not a task of a valid plan: read nothing
+    const int first = t0 / P + wave;
+    const int pg_end = (t1 + P - 1) / P;
+    const int npw = first < pg_end ? (pg_end - first + W - 1) / W : 0;
+    const int nunits = npw * NH;  // unit u: page u / NH of the wave, head g + u % NH
+    const int* idrow = a.block_table + (size_t)row * a.max_pages_per_row + first;
+    auto fetch_ids = [&](int base) {  // ids of the wave's pages base .. base + 63
+      return lane < npw - base ? idrow[(size_t)(base + lane) * W] : 0;
+    };
+    int ids = fetch_ids(0);
+    auto issue = [&](v4u (&kr)[4], v4u (&vr)[4], int u) {  // u >= nunits: empty descriptors
+      const int j = u / NH, hh = u - (u / NH) * NH;
+      int phys = __builtin_amdgcn_readlane(ids, j & 63);
+      const bool ok = u < nunits && phys >= 0 && phys < a.num_pages;
+      phys = uniform(ok ? phys : 0);
+      const int bytes = uniform(ok ? page_bytes : 0);
+      const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, bytes);
+      const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, bytes);
+      const int k_off = col * tok_b + (g + hh) * D * 2 + grp * 16;
+      const int v_off = grp * tok_b + (g + hh) * D * 2 + col * 16;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) kr[c] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, k_off, c * 64, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, v_off, i * 4 * tok_b, 0);
+    };
+    auto fold = [&](const v4u (&kr)[4], const v4u (&vr)[4]) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) x += (kr[c].x ^ kr[c].y ^ kr[c].z ^ kr[c].w) + (vr[c].x ^ vr[c].y ^ vr[c].z ^ vr[c].w);
+    };
+    v4u ka[4], va[4], kb[4], vb[4];
+    issue(ka, va, 0);
+    issue(kb, vb, 1);
+    for (int u = 0; u < nunits; u += 2) {
+      fold(ka, va);
+      // unit u + 2 is the first head of a page; a new block of 64 ids starts there
+      if (u + 2 < nunits && ((u + 2) / NH) % 64 == 0) ids = fetch_ids((u + 2) / NH);
+      issue(ka, va, u + 2);
+      fold(kb, vb);
+      issue(kb, vb, u + 3);
+    }
+  }
+  hold[threadIdx.x] = x;
+  __syncthreads();
+  if (hold[(threadIdx.x + 1) % (W * 64)] == 0x9E3779B9u) *a.sink = x;  // keeps the loads; practically never taken
+}
+
 // Workgroups of `kernel` resident on the current device at once (occupancy x CUs),
 // at least one per CU. The split kernels loop over tasks with the grid as stride, so
 // their grid is the task bound capped at this count (taken once per kernel, on the
@@ -1753,6 +1829,22 @@ hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_
   hipExtLaunchKernelGGL(read_kernel, dim3((unsigned)blocks), dim3(256), 0, s, start, stop, 0, (const uint4*)src, n,
                         sink);
   return hipGetLastError();
+}
+
+// The decode kernel's grid: the task bound (in NH-task units) capped at one workgroup
+// per compute unit.
+hipError_t launch_page_read(const PageReadArgs& a, int heads_per_workgroup, hipStream_t s, hipEvent_t start,
+                            hipEvent_t stop) {
+  auto go = [&](auto kernel, int nh) {
+    static_assert(kWaves * 64 <= kPageReadHoldWords, "hold covers the workgroup");
+    const int resident = resident_blocks((const void*)kernel, kWaves * 64);
+    const int units = a.max_tasks / nh > 0 ? a.max_tasks / nh : 1;
+    const int grid = units < resident ? units : resident;
+    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kWaves * 64), 0, s, start, stop, 0, a);
+    return hipGetLastError();
+  };
+  if (heads_per_workgroup == 2) return go(page_read_kernel<kWaves, 2>, 2);
+  return go(page_read_kernel<kWaves, 1>, 1);
 }
 
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t s) {

@@ -142,6 +142,27 @@ def test_copy_and_init_validation():
     assert L.pkv_check_device_status(0, None, None) == pkv.PKV_ERR_INVALID_ARG
 
 
+def test_stream_read_pages_validation():
+    L = lib()
+
+    def rp(**kw):
+        a = dict(k=FAKE, num_pages=100, maxp=10, B=2, hkv=8, d=128, tasks=FAKE, max_tasks=64, hpw=1, sink=FAKE)
+        a.update(kw)
+        return L.pkv_stream_read_pages(a["k"], FAKE, a["num_pages"], FAKE, a["maxp"], a["B"], a["hkv"], a["d"],
+                                       a["tasks"], FAKE, a["max_tasks"], a["hpw"], a["sink"], None, None, None)
+    assert rp(k=0) == pkv.PKV_ERR_INVALID_ARG
+    assert rp(k=FAKE + 8) == pkv.PKV_ERR_INVALID_ARG          # K not 16-byte aligned
+    assert rp(tasks=0) == pkv.PKV_ERR_INVALID_ARG
+    assert rp(sink=FAKE + 2) == pkv.PKV_ERR_INVALID_ARG
+    assert rp(num_pages=0) == pkv.PKV_ERR_INVALID_ARG
+    assert rp(max_tasks=0) == pkv.PKV_ERR_INVALID_ARG
+    assert rp(hkv=257) == pkv.PKV_ERR_INVALID_ARG
+    assert rp(hpw=3) == pkv.PKV_ERR_INVALID_ARG
+    assert rp(hpw=2, hkv=3) == pkv.PKV_ERR_INVALID_ARG         # pairs need an even head count
+    assert rp(maxp=1 << 28) == pkv.PKV_ERR_INVALID_ARG         # maxp * 16 beyond int32
+    assert rp(d=64) == pkv.PKV_ERR_UNSUPPORTED
+
+
 def test_plan_decode_validation():
     L = lib()
 
