@@ -758,15 +758,15 @@ struct MfmaTask {
     first = uniform(t0 / P + wave);
     npw = uniform(first < pg_end ? (pg_end - first + W - 1) / W : 0);
     bad = false;
-    const bool hv = col < G;
+    // Q of the NH * G query heads through one buffer descriptor; lanes past the G heads
+    // (MFMA columns G..15) read at an offset past its end, which returns zeros, so the
+    // loads carry no branch and the page-id load below need not wait for them.
+    const __amdgpu_buffer_rsrc_t q_rsrc = page_rsrc(a.q + ((size_t)row * a.Hq + (size_t)g * G) * D, NH * G * D * 2);
 #pragma unroll
     for (int hh = 0; hh < NH; ++hh) {
-      const uint16_t* qh = a.q + ((size_t)row * a.Hq + (size_t)(g + hh) * G + (hv ? col : 0)) * D;
+      const int qoff = col < G ? ((hh * G + col) * D + 8 * grp) * 2 : kOutOfRange;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const v4u z = {0u, 0u, 0u, 0u};
-        qb[hh][c] = hv ? *reinterpret_cast<const v4u*>(qh + c * 32 + 8 * grp) : z;
-      }
+      for (int c = 0; c < 4; ++c) qb[hh][c] = __builtin_amdgcn_raw_buffer_load_b128(q_rsrc, qoff, c * 64, 0);
     }
     ids = lane < npw ? a.block_table[(size_t)row * a.max_pages_per_row + first + lane * W] : 0;
   }
@@ -1083,9 +1083,26 @@ constexpr int kCandidateRows = 16;  // batches up to this size test several quot
 // `n` is seq_lens[lane] (0 for lanes >= B), loaded by the caller.
 __device__ __forceinline__ bool wave_plan(const PlanArgs& a) { return a.B <= 64 && !a.block_table; }
 
+// seq_lens[lane] (0 for lanes >= B) through scalar loads (uniform addresses): they wait
+// on their own counter, not behind the wave's vector loads, so the planner can start as
+// soon as the lengths arrive while the task's first loads are still in flight.
+// (Loads through the constant address space with uniform addresses are scalar loads; the
+// index is clamped to the batch instead of branched on, so the loads of a group of 16 are
+// issued together.)
+typedef const __attribute__((address_space(4))) int32_t const_i32;
 __device__ __forceinline__ int wave_plan_len(const PlanArgs& a) {
   const int lane = threadIdx.x & 63;
-  return lane < a.B ? a.seq_lens[lane] : 0;
+  const int B = uniform(a.B);
+  const const_i32* lens = (const const_i32*)a.seq_lens;
+  int n = 0;
+  for (int i0 = 0; i0 < B; i0 += 16) {
+    int v[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v[j] = lens[min(i0 + j, B - 1)];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) n = (lane == i0 + j && i0 + j < B) ? v[j] : n;
+  }
+  return n;
 }
 
 __device__ __forceinline__ void plan_compute_wave(const PlanArgs& a, const PlanLds& L, bool report, int n) {
@@ -1427,11 +1444,20 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       // batch's bounds (the buffer may hold anything on the first call), and the begun
       // loads are kept only if the new plan gives this workgroup a task they cover;
       // otherwise the task is begun again. The results never depend on the hint.
-      const int n_raw = threadIdx.x < 64 ? wave_plan_len(a.plan) : 0;  // the planner's load goes first
-      if (NH * (int)blockIdx.x < a.max_tasks) {
+      // The hint's loads go out first; wave 0 then loads the lengths with scalar loads
+      // while they travel, and the planner waits only for those.
+      const bool has_hint = NH * (int)blockIdx.x < a.max_tasks;
+      int hv[4] = {-1, -1, -1, -1};
+      if (has_hint) {
         const int* tp = reinterpret_cast<const int*>(a.tasks + NH * blockIdx.x);
-        const int hr = uniform(ld_i32<true>(tp + 0)), hg = uniform(ld_i32<true>(tp + 1));
-        const int h0 = uniform(ld_i32<true>(tp + 3)), h1 = uniform(ld_i32<true>(tp + 4));
+        hv[0] = ld_i32<true>(tp + 0);
+        hv[1] = ld_i32<true>(tp + 1);
+        hv[2] = ld_i32<true>(tp + 3);
+        hv[3] = ld_i32<true>(tp + 4);
+      }
+      const int n_raw = threadIdx.x < 64 ? wave_plan_len(a.plan) : 0;
+      if (has_hint) {
+        const int hr = uniform(hv[0]), hg = uniform(hv[1]), h0 = uniform(hv[2]), h1 = uniform(hv[3]);
         if (hr >= 0 && hr < a.B && hg >= 0 && hg % NH == 0 && hg + NH <= a.Hkv && h0 >= 0 && h1 > h0 &&
             h1 <= a.max_pages_per_row * P) {
           body.begin(a, hr, hg, h0, h1);
