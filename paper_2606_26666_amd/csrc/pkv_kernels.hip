@@ -488,7 +488,8 @@ __device__ __forceinline__ void finish_task(const DecodeArgs& a, int slot, float
 // first loads before its plan is known (split_kernel):
 //   begin(row, g, t0, t1)  loads Q and the wave's first 64 page ids
 //   prime()                issues the loads of the wave's first two pages (waits for the ids)
-//   run(t1, slot)          the page loop, then the task's partial state into `slot`
+//   run(last_t1)           the page loop, then the wave states in LDS (finish_task and
+//                          the fused route combine them into the task's partial state)
 // covers(row, g, t0, t1) tells whether a begun task read exactly what task (row, g, t0,
 // t1) reads in those phases: the same row, head and first token and the same page
 // count. t1 itself only masks tokens of the last page, which run() applies.
@@ -555,8 +556,12 @@ struct ValuTask {
     issue(a, kb, vb, 1, npw > 1);
   }
 
-  template <bool COHERENT>
-  __device__ __forceinline__ void run(const DecodeArgs& a, int t1, int slot, float* lds) {
+  // `plan` (KnownTask or SpecTask) gives the row's token count for the task's last page
+  // (last_t1, called only by the wave that holds that page, just before consuming it)
+  // and tells whether the task was dropped (a speculative run that the plan did not
+  // confirm: the wave stops, and its state is discarded).
+  template <typename PlanView>
+  __device__ __forceinline__ void run(const DecodeArgs& a, PlanView& plan, float* lds) {
     float* lds_m = lds;                // [W][G]
     float* lds_l = lds + W * G;        // [W][G]
     float* lds_acc = lds + 2 * W * G;  // [W][G][D]
@@ -583,6 +588,7 @@ struct ValuTask {
 #pragma unroll
         for (int h = 0; h < G; ++h) x[h][i] = row_sum16(dot8(q[h], kr[i])) * a.scale_log2;
       }
+      const int t1 = pg == pg_end - 1 ? plan.last_t1() : pg_end * P;  // pages before the last are whole
       if (pg * P + P > t1) {  // the row's last, partial page: mask tokens >= t1
         const int tok = pg * P + r;  // this lane row's token in load i is tok + 4i
 #pragma unroll
@@ -632,7 +638,8 @@ struct ValuTask {
     // current page is scored and accumulated. Inside the steady-state loop every load is
     // unconditional, so each consume waits only for its own buffer's loads. begin() and
     // prime() have fetched the first id block and issued the first two pages.
-    for (int k0 = 0; k0 < npw; k0 += 64) {
+    bool dropped = false;
+    for (int k0 = 0; k0 < npw && !dropped; k0 += 64) {
       const int n = min(64, npw - k0);
       if (k0 > 0) {  // begin() and prime() did this for the first id block
         ids = (k0 + lane < npw) ? a.block_table[(size_t)row * a.max_pages_per_row + first + (k0 + lane) * W] : 0;
@@ -642,11 +649,13 @@ struct ValuTask {
       // pages j (ka) and j + 1 (kb) are in flight at the top of each iteration
       int j = 0;
       for (; j + 2 < n; j += 2) {
+        if ((dropped = plan.dropped())) break;
         consume(ka, va, k0 + j);
         issue(a, ka, va, j + 2, true);
         consume(kb, vb, k0 + j + 1);
         issue(a, kb, vb, (j + 3) & 63, j + 3 < n);
       }
+      if (dropped) break;
       consume(ka, va, k0 + j);
       if (j + 1 < n) consume(kb, vb, k0 + j + 1);
     }
@@ -690,7 +699,6 @@ struct ValuTask {
       lds_bad[wave] = bad ? 1 : 0;
     }
     __syncthreads();
-    finish_task<G, W, COHERENT>(a, slot, lds);
   }
 };
 
@@ -704,12 +712,17 @@ struct ValuTask {
 //   O^T[128 x 16] += V_page^T[128 x 16 tokens] . P^T[16 tokens x 16]   (16 x mfma 16x16x16 f16:
 //                                                                      P as hi + lo halves)
 // Lane (grp, col) = (lane / 16, lane % 16):
-//   K operand   token col, dims [32 c + 8 grp, +8): one 16-byte load per c, native layout
+//   K operand   token col, dims [32 c + 8 grp, +8): K is read as V is, four 1 KiB loads
+//               of four whole 256-byte head rows each (lane: token 4 i + grp, dims
+//               [8 col, +8)), staged token-major in LDS and read back in this layout
+//               (on MI355X, whole-row reads stream 2-4% faster than 64-byte pieces)
 //   Q operand   head col, dims [32 c + 8 grp, +8) (zero for col >= G), loaded once
 //   scores      tokens 4 grp + r (r = 0..3) of head col, which is also the P operand
 //   V operand   dims 16 db + col, tokens 4 grp + r: V is staged token-major in LDS and
 //               read back transposed with ds_read_b64_tr_b16 (within 16 lanes, lane i
 //               receives element i % 4 of the rows that lanes 4 j + i / 4 address)
+// The staged rows are padded (K to 272 bytes, V to 288) so that the lanes of one LDS
+// pass address distinct banks.
 //   output      dims 16 db + 4 grp + r of head col
 // Every value a lane holds belongs to head col, so the online-softmax max (shared by the
 // four groups of a head, per page) and the rescale are per lane.
@@ -717,6 +730,16 @@ typedef _Float16 h8v __attribute__((ext_vector_type(8)));
 typedef _Float16 h4v __attribute__((ext_vector_type(4)));
 typedef short s4v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s4v lds_s4v;
+
+// Per wave, one K and one V page of one head staged in LDS: 16 rows of 256 bytes each,
+// padded (pitches in 16-byte units). One allocation per kernel, whatever the callers.
+constexpr int kKPitch = D / 8 + 1, kVPitch = D / 8 + 2;
+constexpr int kStageUnits = P * (kKPitch + kVPitch);
+template <int W>
+__device__ __forceinline__ v4u* kv_stage() {
+  __shared__ v4u stage[W * kStageUnits];
+  return stage;
+}
 
 // The matrix-core body runs G > PKV_VALU_BODY_MAX_G (default: G = 4 and 8). A library
 // built with -DPKV_VALU_BODY_MAX_G=4 (or 8) runs the VALU body up to that G instead: an
@@ -787,8 +810,7 @@ struct MfmaTask {
     const size_t tok_stride = (size_t)a.Hkv * D;  // halves between consecutive tokens
     const size_t page_stride = (size_t)P * tok_stride;
     const int tok_b = (int)(tok_stride * 2);
-    const int k_off = col * tok_b + (g + hh) * D * 2 + grp * 16;  // + 64 c
-    const int v_off = grp * tok_b + (g + hh) * D * 2 + col * 16;  // + 4 i tok_b
+    const int kv_off = grp * tok_b + (g + hh) * D * 2 + col * 16;  // + 4 i tok_b (K and V alike)
     const bool ok = phys >= 0 && phys < a.num_pages;
     bad |= live && !ok;
     const int page_bytes = uniform(live ? (int)(page_stride * 2) : 0);
@@ -796,9 +818,9 @@ struct MfmaTask {
     const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, page_bytes);
     const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, page_bytes);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) kr[c] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, k_off, c * 64, 0);
+    for (int i = 0; i < 4; ++i) kr[i] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, kv_off, i * 4 * tok_b, 0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, v_off, i * 4 * tok_b, 0);
+    for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, kv_off, i * 4 * tok_b, 0);
   }
 
   // Both issues are unconditional (pages past the wave's count are not live), so every
@@ -814,9 +836,8 @@ struct MfmaTask {
     }
   }
 
-  template <bool COHERENT>
-  __device__ __forceinline__ void run(const DecodeArgs& a, int t1, int slot, float* lds) {
-    __shared__ v4u vstage[W][P * D / 8];  // one V page of one head per wave: 16 rows of 256 B
+  template <typename PlanView>
+  __device__ __forceinline__ void run(const DecodeArgs& a, PlanView& plan, float* lds) {
     float* lds_m = lds;                     // [NH][W][G]
     float* lds_l = lds + NH * W * G;        // [NH][W][G]
     float* lds_acc = lds + 2 * NH * W * G;  // [NH][W][G][D]
@@ -835,25 +856,30 @@ struct MfmaTask {
 #pragma unroll
       for (int db = 0; db < D / 16; ++db) acc[hh][db] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
     }
-    v4u* vst = &vstage[wave][0];
-    const int tr_off = (4 * grp + (col >> 2)) * (D * 2) + (col & 3) * 8;  // + 32 db
+    v4u* kst = kv_stage<W>() + wave * kStageUnits;
+    v4u* vst = kst + P * kKPitch;
+    const int tr_off = (4 * grp + (col >> 2)) * (kVPitch * 16) + (col & 3) * 8;  // + 32 db
 
     // one page of one head into that head's state (m, l, acc) with its query block qh
     auto consume = [&](v4u (&kr)[4], v4u (&vr)[4], int k, float& m, float& l, v4f (&acc)[D / 16],
                        const v4u (&qh)[4]) {
       const int pg = first + k * W;
+      const int t1 = pg == pg_end - 1 ? plan.last_t1() : pg_end * P;  // pages before the last are whole
       const bool tail = pg * P + P > t1;  // the row's last, partial page
+      // K token-major into LDS, read back as the A operand (token col, dims 32 c + 8 grp)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) kst[(4 * i + grp) * kKPitch + col] = kr[i];
       v4f sc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
       for (int c = 0; c < 4; ++c)
-        sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kr[c]), __builtin_bit_cast(h8v, qh[c]),
-                                                    sc, 0, 0, 0);
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8v, kst[col * kKPitch + 4 * c + grp]),
+                                                    __builtin_bit_cast(h8v, qh[c]), sc, 0, 0, 0);
       // stage V token-major; rows past t1 are zeroed (their p is 0, but 0 * NaN is not)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         v4u v = vr[i];
         if (tail && pg * P + 4 * i + grp >= t1) v = v4u{0u, 0u, 0u, 0u};
-        vst[(4 * i + grp) * (D / 8) + col] = v;
+        vst[(4 * i + grp) * kVPitch + col] = v;
       }
       float x[4];
 #pragma unroll
@@ -893,7 +919,8 @@ struct MfmaTask {
       }
     };
 
-    for (int k0 = 0; k0 < npw; k0 += 64) {
+    bool dropped = false;
+    for (int k0 = 0; k0 < npw && !dropped; k0 += 64) {
       const int n = min(64, npw - k0);
       if constexpr (NH == 1) {
         if (k0 > 0) {  // begin() and prime() did this for the first id block
@@ -904,11 +931,13 @@ struct MfmaTask {
         // pages j (ka) and j + 1 (kb) are in flight at the top of each iteration
         int j = 0;
         for (; j + 2 < n; j += 2) {
+          if ((dropped = plan.dropped())) break;
           consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
           issue(a, ka, va, j + 2, true);
           consume(kb, vb, k0 + j + 1, m[0], l[0], acc[0], qb[0]);
           issue(a, kb, vb, (j + 3) & 63, j + 3 < n);
         }
+        if (dropped) break;
         consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
         if (j + 1 < n) consume(kb, vb, k0 + j + 1, m[0], l[0], acc[0], qb[0]);
       } else {
@@ -920,11 +949,13 @@ struct MfmaTask {
         // page j of both heads is in flight at the top of each iteration
         int j = 0;
         for (; j + 1 < n; ++j) {
+          if ((dropped = plan.dropped())) break;
           consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
           issue(a, ka, va, j + 1, true, 0);
           consume(kb, vb, k0 + j, m[NH - 1], l[NH - 1], acc[NH - 1], qb[NH - 1]);
           issue(a, kb, vb, j + 1, true, 1);
         }
+        if (dropped) break;
         consume(ka, va, k0 + j, m[0], l[0], acc[0], qb[0]);
         consume(kb, vb, k0 + j, m[NH - 1], l[NH - 1], acc[NH - 1], qb[NH - 1]);
       }
@@ -949,8 +980,14 @@ struct MfmaTask {
     }
     if (lane == 0) lds_bad[wave] = bad ? 1 : 0;
     __syncthreads();
-    finish_task<G, W, COHERENT, NH>(a, slot, lds);
   }
+};
+
+// What a task body's run() needs from the plan. KnownTask: the task is the plan's.
+struct KnownTask {
+  int t1;
+  __device__ __forceinline__ int last_t1() const { return t1; }
+  __device__ __forceinline__ bool dropped() const { return false; }
 };
 
 // The task body each route runs: matrix-core products for G = 4 and 8, VALU otherwise
@@ -973,7 +1010,9 @@ __device__ __forceinline__ void run_split_task(const DecodeArgs& a, int row, int
   TaskBody<G, W> body;
   body.begin(a, row, g, t0, t1);
   body.prime(a);
-  body.template run<COHERENT>(a, t1, slot, lds);
+  KnownTask known{t1};
+  body.run(a, known, lds);
+  finish_task<G, W, COHERENT>(a, slot, lds);
 }
 
 template <int G>
@@ -1366,6 +1405,37 @@ __device__ __forceinline__ TaskRec plan_task(const PlanArgs& a, const PlanLds& L
   return TaskRec{lo, k % a.Hkv, sp, b0 * T, min(b1 * T, n)};
 }
 
+// The one-launch route's speculative run of the hinted task (row hr, KV head hg, first
+// token h0, h_pages pages) while wave 0 plans. Once the plan is in LDS (flag `ready`),
+// the verdict is the plan's t1 for this workgroup's first task (index `task`) if that
+// task is the hinted one (same row, KV head, first token and page count), else -1: the
+// run is dropped. dropped() looks without waiting; last_t1() waits for the plan.
+struct SpecTask {
+  const PlanArgs& pa;
+  PlanLds PL;
+  const int* ready;
+  int task, hr, hg, h0, h_pages;
+  int verdict = -2;  // -2: plan not seen yet
+  __device__ __forceinline__ void judge() {
+    verdict = -1;
+    if (task < plan_wave_tasks(pa, PL, false)) {
+      const TaskRec r = plan_task(pa, PL, task);
+      if (r.row == hr && r.g == hg && r.t0 == h0 && (r.t1 + P - 1) / P == h_pages) verdict = r.t1;
+    }
+  }
+  __device__ __forceinline__ bool dropped() {
+    if (verdict == -2 && __hip_atomic_load(ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) != 0) judge();
+    return verdict == -1;
+  }
+  __device__ __forceinline__ int last_t1() {
+    if (verdict == -2) {
+      while (__hip_atomic_load(ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == 0) __builtin_amdgcn_s_sleep(1);
+      judge();
+    }
+    return verdict;
+  }
+};
+
 // The planner's outputs: split_offsets, num_tasks, the task list and zeroed completion
 // counters.
 template <int NT, bool COHERENT>
@@ -1431,42 +1501,59 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   // and at the end of the last task).
   asm volatile("" ::"s"(a.q), "s"(a.partials), "s"(gridDim.x));
   TaskBody<G, W, NH> body;
-  bool begun = false;  // this wave's body holds a task begun before the plan
+  bool begun = false;  // the workgroup's body holds a task begun before the plan
   int plan_ntasks = 0;
+  __shared__ int plan_ready;  // wave planner: set once wave 0 has put the plan in LDS
+  // The speculative run is for one-head workgroups: with KV-head pairs its extra live
+  // state pushed the kernel past 256 registers per lane (spills in the page loop, 50%
+  // slower on the B8 traces), so a pair's hinted task is only begun and primed.
+  constexpr bool kSpecRun = NH == 1;
   if (PLAN) {
     if (wave_plan(a.plan)) {
       // Speculative start. Between decode steps a plan rarely changes (lengths grow by a
-      // token), so while wave 0 runs the planner, each wave begins and primes the task
-      // listed at this workgroup's index (NH = 2: the pair's first task, at twice the
-      // index) in the task list left by the previous launch (the task it ran then): a
-      // hint, read with agent-scope loads because workgroup 0
-      // rewrites the list meanwhile. A record is used only if it names a task inside the
-      // batch's bounds (the buffer may hold anything on the first call), and the begun
-      // loads are kept only if the new plan gives this workgroup a task they cover;
-      // otherwise the task is begun again. The results never depend on the hint.
-      // The hint's loads go out first; wave 0 then loads the lengths with scalar loads
-      // while they travel, and the planner waits only for those.
+      // token), so while wave 0 runs the planner, each wave begins, primes and runs the
+      // task listed at this workgroup's index (NH = 2: the pair's first task, at twice
+      // the index) in the task list left by the previous launch (the task it ran then):
+      // a hint, read with agent-scope loads because workgroup 0 rewrites the list during
+      // the launch. A record is used only if it names a task inside the batch's bounds
+      // (the buffer may hold anything on the first call). Every page of the hinted task
+      // but its last is read and accumulated without the plan: their tokens do not depend
+      // on it. The wave that holds the last page waits there for the plan, which gives the
+      // row's token count for its masking, and the run's result is kept only if the plan
+      // gives this workgroup a task with the same row, KV head, first token and page
+      // count; otherwise the task is run again from the start. Results never depend on
+      // the hint. The hint's loads go out first; wave 0 then loads the lengths with
+      // scalar loads while they travel, and the planner waits only for those.
+      if (threadIdx.x == 0) plan_ready = 0;
+      __syncthreads();
       const bool has_hint = NH * (int)blockIdx.x < a.max_tasks;
       int hv[4] = {-1, -1, -1, -1};
       if (has_hint) {
-        const int* tp = reinterpret_cast<const int*>(a.tasks + NH * blockIdx.x);
+        const int* tp = reinterpret_cast<const int*>(a.tasks + NH * (int)blockIdx.x);
         hv[0] = ld_i32<true>(tp + 0);
         hv[1] = ld_i32<true>(tp + 1);
         hv[2] = ld_i32<true>(tp + 3);
         hv[3] = ld_i32<true>(tp + 4);
       }
       const int n_raw = threadIdx.x < 64 ? wave_plan_len(a.plan) : 0;
-      if (has_hint) {
-        const int hr = uniform(hv[0]), hg = uniform(hv[1]), h0 = uniform(hv[2]), h1 = uniform(hv[3]);
-        if (hr >= 0 && hr < a.B && hg >= 0 && hg % NH == 0 && hg + NH <= a.Hkv && h0 >= 0 && h1 > h0 &&
-            h1 <= a.max_pages_per_row * P) {
-          body.begin(a, hr, hg, h0, h1);
-          begun = true;
-        }
+      const int hr = uniform(hv[0]), hg = uniform(hv[1]), h0 = uniform(hv[2]), h1 = uniform(hv[3]);
+      if (has_hint && hr >= 0 && hr < a.B && hg >= 0 && hg % NH == 0 && hg + NH <= a.Hkv && h0 >= 0 && h1 > h0 &&
+          h1 <= a.max_pages_per_row * P) {
+        body.begin(a, hr, hg, h0, h1);
+        begun = true;
       }
-      if (threadIdx.x < 64) plan_compute_wave(a.plan, PL, blockIdx.x == 0, n_raw);
+      if (threadIdx.x < 64) {
+        plan_compute_wave(a.plan, PL, blockIdx.x == 0, n_raw);
+        __hip_atomic_store(&plan_ready, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
       body.prime(a);  // nothing to issue when no task was begun (npw = 0)
-      __syncthreads();
+      if (begun && kSpecRun) {
+        SpecTask spec{a.plan, PL, &plan_ready, NH * (int)blockIdx.x, hr, hg, h0, (h1 + P - 1) / P};
+        body.run(a, spec, lds);
+        // the run ended with a workgroup barrier: wave 0's plan is visible to every wave
+      } else {
+        __syncthreads();
+      }
       plan_ntasks = plan_wave_tasks(a.plan, PL, blockIdx.x == 0);
     } else {
       plan_ntasks = plan_compute<W * 64>(a.plan, PL, blockIdx.x == 0);
@@ -1491,25 +1578,17 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       rec[3] = tp[4];
     }
   };
-  if (!PLAN || NH * (int)blockIdx.x < plan_ntasks) fetch(NH * blockIdx.x);  // PLAN: only real tasks
+  if (!PLAN || NH * (int)blockIdx.x < plan_ntasks) fetch(NH * (int)blockIdx.x);  // PLAN: only real tasks
   int ntasks = PLAN ? plan_ntasks : uniform(*a.num_tasks);
   if (ntasks > a.max_tasks) ntasks = a.max_tasks;
-  // Task t (record in rec) on body `bd`, which holds a begun task when `keep`: the loads
-  // it began are used if they cover task t, else the task is begun again.
-  auto task = [&](TaskBody<G, W, NH>& bd, int t, bool keep) {
-    const int row = uniform(rec[0]), g = uniform(rec[1]);
-    const int t0 = uniform(rec[2]), t1 = uniform(rec[3]);
-    if (row < 0 || row >= a.B || g < 0 || g % NH != 0 || g + NH > a.Hkv || t0 < 0 || t1 <= t0 ||
-        t1 > a.max_pages_per_row * P) {  // not a task of a valid plan: flag and skip
-      if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
-      return;
-    }
-    if (!(keep && bd.covers(row, g, t0, t1))) {
-      bd.begin(a, row, g, t0, t1);
-      bd.prime(a);
-    }
-    bd.template run<FUSED>(a, t1, t, lds);
-    if (FUSED) {
+  // The end of task t (KV heads g .. g + NH - 1 of `row`): its partial state from the
+  // wave states in LDS; on the fused route, the completion count and the last
+  // arriver's merge.
+  auto finish = [&](int t, int row, int g) __attribute__((always_inline)) {
+    if (!FUSED) {
+      finish_task<G, W, false, NH>(a, t, lds);
+    } else {
+      finish_task<G, W, true, NH>(a, t, lds);
       const int off = uniform(PLAN ? PL.off[row] : a.split_offsets[row]);
       int nsplit = uniform(PLAN ? PL.off[row + 1] : a.split_offsets[row + 1]) - off;
       if (off < 0 || nsplit < 1 || (long long)(off + nsplit) * a.Hkv > a.max_tasks) {
@@ -1537,11 +1616,34 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
     }
     __syncthreads();
   };
-  // The first task is the only one a speculative start can have begun; later tasks run
-  // on a body of their own, so the first body's registers are free after its task.
-  // NH = 2: the plan's task count is Hkv times its split count, and Hkv is even.
-  int t = NH * blockIdx.x;
-  if (t + NH <= ntasks) task(body, t, begun);
+  // Task t (record in rec) on body `bd`, which holds a begun task when `keep`: the loads
+  // it began are used if they cover task t, else the task is begun again.
+  auto task = [&](TaskBody<G, W, NH>& bd, int t, bool keep) __attribute__((always_inline)) {
+    const int row = uniform(rec[0]), g = uniform(rec[1]);
+    const int t0 = uniform(rec[2]), t1 = uniform(rec[3]);
+    if (row < 0 || row >= a.B || g < 0 || g % NH != 0 || g + NH > a.Hkv || t0 < 0 || t1 <= t0 ||
+        t1 > a.max_pages_per_row * P) {  // not a task of a valid plan: flag and skip
+      if (threadIdx.x == 0) atomicOr(a.err, (unsigned)PKV_DEVERR_TASK);
+      return;
+    }
+    if (!(keep && bd.covers(row, g, t0, t1))) {
+      bd.begin(a, row, g, t0, t1);
+      bd.prime(a);
+    }
+    KnownTask known{t1};
+    bd.run(a, known, lds);
+    finish(t, row, g);
+  };
+  // The first task is the only one a speculative start can have begun (and run); later
+  // tasks run on a body of their own, so the first body's registers are free after its
+  // task. NH = 2: the plan's task count is Hkv times its split count, and Hkv is even.
+  int t = NH * (int)blockIdx.x;
+  if (t + NH <= ntasks) {
+    if (begun && kSpecRun && body.covers(uniform(rec[0]), uniform(rec[1]), uniform(rec[2]), uniform(rec[3])))
+      finish(t, uniform(rec[0]), uniform(rec[1]));  // the speculative run was this task
+    else
+      task(body, t, begun && !kSpecRun);  // a begun task that has not run keeps its loads if they cover t
+  }
   for (t += NH * gridDim.x; t + NH <= ntasks; t += NH * gridDim.x) {
     fetch(t);
     TaskBody<G, W, NH> next;
@@ -1643,7 +1745,7 @@ __global__ __launch_bounds__(256) void read_kernel(const uint4* __restrict__ src
 // list (records as the planner writes them), the waves of a workgroup read the K and V
 // bytes of the task's NH KV heads over its pages as the decode body does (wave w takes
 // pages w, w + W, ... of the task, page ids fetched 64 at a time, per page and head four
-// 16-byte buffer loads of K in the matrix-core body's K layout and four of V; two
+// 16-byte buffer loads of K and four of V, each covering four whole 256-byte rows; two
 // (page, head) units in flight per wave: two pages of one head, or one page of each of
 // two heads), with the decode's grid (one workgroup per compute unit, held by the LDS
 // reservation) and task-to-workgroup mapping. Nothing else: no queries, no arithmetic
@@ -1687,12 +1789,11 @@ __global__ __launch_bounds__(W * 64) void page_read_kernel(PageReadArgs a) {
       const int bytes = uniform(ok ? page_bytes : 0);
       const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, bytes);
       const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, bytes);
-      const int k_off = col * tok_b + (g + hh) * D * 2 + grp * 16;
-      const int v_off = grp * tok_b + (g + hh) * D * 2 + col * 16;
+      const int kv_off = grp * tok_b + (g + hh) * D * 2 + col * 16;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) kr[c] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, k_off, c * 64, 0);
+      for (int i = 0; i < 4; ++i) kr[i] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, kv_off, i * 4 * tok_b, 0);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, v_off, i * 4 * tok_b, 0);
+      for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, kv_off, i * 4 * tok_b, 0);
     };
     auto fold = [&](const v4u (&kr)[4], const v4u (&vr)[4]) {
 #pragma unroll
