@@ -194,99 +194,102 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
   const int my_hh = myh / G, my_h = myh % G;
   auto soff = [&](int s, int hh) { return (slot0 + s * stride + hh) * SB; };
 
-  // At most four runs (32 splits): the four lanes of each DPP quad hold runs 0-3 of the
-  // same CPT float4 columns (lane r: run r, i.e. splits 8r..8r+7), so the maximum, the
-  // marker and the run sums are exchanged inside the quad, with no LDS and no barrier.
-  // A wave's 16 CPT columns lie in at most two query heads (one for CPT <= 2); lane j of
-  // the wave loads (m, l) of split j % 32 of the wave's head j / 32 in one 8-byte load,
-  // and each lane takes those of its run's eight splits by lane shuffles. Per wave that
-  // is 1 + 8 CPT vector loads, all in flight together. The operations and their order
-  // are those of the general path below.
+  // At most four runs (32 splits): column path. Column thread c (< GH * D / 4) owns the
+  // four output elements 4c .. 4c + 3, so lanes 0-31 of a wave hold one query head's D
+  // columns and lanes 32-63 the next head's (GH = 1: one head per half-wave). The NT
+  // threads form NG groups of column threads; group i sums runs i * RPG .. i * RPG +
+  // RPG - 1, each in split order from zero, reading its columns from every existing
+  // state of those runs (one 16-byte load per state, none for states that do not exist:
+  // 1 KiB per wave instruction). Lane j of a half loads (m, l) of split j of its half's
+  // head; the maximum and the marker are reduced over the half, and the weights pass
+  // through LDS, which every lane of the half reads at the same address. The run sums
+  // meet in LDS and group 0 adds them in run order, from zero. The operations and their
+  // order are those of the general path below (entries past nsplit in the last run add
+  // 0 * 0), so every path rounds alike.
   if (nsplit <= 4 * kMergeRun) {
-    constexpr int CPT = 4 * E4 > NT ? 4 * E4 / NT : 1;  // float4 columns per thread
-    constexpr int HPW = CPT > 2 ? CPT / 2 : 1;          // query heads per wave
-    static_assert(CPT <= 4 && 4 * E4 <= CPT * NT && HPW * 32 <= 64, "quad merge shape");
-    const int r = lane & 3;
-    const int e40 = (tid >> 2) * CPT;  // this quad's first float4 column
-    const bool active = e40 < E4;
-    const int e4a = active ? e40 : 0;
-    const int hh = e4a / E4H;                   // KV head within the NH merged
-    // (m, l) of split lane % 32 of the wave's query head lane / 32
-    const int wave_e4 = wave * 16 * CPT;        // the wave's first float4 column
-    const int jh = lane >> 5, js = lane & 31;
-    const int e4j = wave_e4 + jh * (D / 4);     // first column of that query head
-    int ml_off = kOutOfRange;
-    if (jh < HPW && e4j < E4 && js < nsplit) {
-      const int hhj = e4j / E4H;
-      ml_off = soff(js, hhj) + (G * D + 2 * (((e4j - hhj * E4H) * 4) / D)) * 4;
-    }
-    const v2f ml = ld_state2<COHERENT>(pr, ml_off);
-    v4f vq[CPT][kMergeRun];
-#pragma unroll
-    for (int u = 0; u < kMergeRun; ++u) {  // a state that does not exist reads as zero
-      const int sidx = r * kMergeRun + u;
-      const int off = sidx < nsplit ? soff(sidx, hh) : kOutOfRange;
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) vq[c][u] = ld_state4<COHERENT>(pr, off + (e4a - hh * E4H + c) * 16);
-    }
-    const int src0 = (HPW > 1 ? ((e4a - wave_e4) * 4 / D) * 32 : 0) + r * kMergeRun;  // lane of the run's first split
-    float mq[kMergeRun], lq[kMergeRun];
-#pragma unroll
-    for (int u = 0; u < kMergeRun; ++u) {
-      mq[u] = __shfl(ml.x, src0 + u);
-      lq[u] = __shfl(ml.y, src0 + u);
-    }
-    float M = kNegInf, bd = 0.0f;
-#pragma unroll
-    for (int u = 0; u < kMergeRun; ++u) {
-      const bool ok = r * kMergeRun + u < nsplit;
-      M = fmaxf(M, ok ? mq[u] : kNegInf);
-      bd = fmaxf(bd, ok && lq[u] < 0.0f ? 1.0f : 0.0f);
-    }
-    M = fmaxf(M, dpp<0xB1>(M));  // quad_perm [1,0,3,2]
-    M = fmaxf(M, dpp<0x4E>(M));  // quad_perm [2,3,0,1]
-    bd = fmaxf(bd, dpp<0xB1>(bd));
-    bd = fmaxf(bd, dpp<0x4E>(bd));
-    const float Mref = (M == kNegInf) ? 0.0f : M;
-    v4f acc[CPT];
-    float lacc = 0.0f;
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) acc[c] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int u = 0; u < kMergeRun; ++u) {
-      const bool ok = r * kMergeRun + u < nsplit;
-      const float w = ok ? ex2(mq[u] - Mref) : 0.0f;
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) {
-        acc[c].x = __builtin_fmaf(w, vq[c][u].x, acc[c].x);
-        acc[c].y = __builtin_fmaf(w, vq[c][u].y, acc[c].y);
-        acc[c].z = __builtin_fmaf(w, vq[c][u].z, acc[c].z);
-        acc[c].w = __builtin_fmaf(w, vq[c][u].w, acc[c].w);
-      }
-      lacc = __builtin_fmaf(w, ok ? lq[u] : 0.0f, lacc);
-    }
-    // run sums added in run order, from zero, as the general path adds them
+    constexpr int kColThreads = GH * D / 4;
+    constexpr int NG = NT / kColThreads >= 4 ? 4 : NT / kColThreads;
+    constexpr int RPG = 4 / NG;                    // runs per group
+    constexpr int kWaves = (NG * kColThreads + 63) / 64;
+    float* rsum = lds + kWaves * 128;              // [run][GH * D] run sums of acc
+    float* rsumL = rsum + 4 * GH * D;              // [run][GH] run sums of l
+    static_assert(D == 128 && NT % kColThreads == 0 && (NG == 1 || NG == 2 || NG == 4), "column merge shape");
+    static_assert(kWaves * 128 + 4 * GH * D + 4 * GH <= merge_lds_floats<G, NH>(), "column merge LDS");
+    const int gi = tid / kColThreads;              // group
+    const int c = tid - gi * kColThreads;          // column thread
+    const int h = c / (D / 4);                     // query head within the GH merged
     const int nrun = (nsplit + kMergeRun - 1) / kMergeRun;
-    auto ordered = [&](float x) {
-      const float x0 = dpp<0x00>(x), x1 = dpp<0x55>(x), x2 = dpp<0xAA>(x), x3 = dpp<0xFF>(x);
-      float t = 0.0f;
-      if (nrun > 0) t += x0;
-      if (nrun > 1) t += x1;
-      if (nrun > 2) t += x2;
-      if (nrun > 3) t += x3;
-      return t;
-    };
-    const float L = ordered(lacc);
-    const bool zero = M == kNegInf || bd != 0.0f;
-    const float iL = 1.0f / L;  // one division per head, then products
+    float M = kNegInf, bd = 0.0f;
+    if (gi < NG) {
+      const int hb = lane >> 5, js = lane & 31;
+      const int hh = h / G;                        // KV head within the NH merged
+      const int ecol = (h % G) * D + (c % (D / 4)) * 4;  // first element in that KV head's acc
+      const int ml_off = js < nsplit ? soff(js, hh) + (G * D + 2 * (h % G)) * 4 : kOutOfRange;
+      const v2f ml = ld_state2<COHERENT>(pr, ml_off);
+      v4f vq[RPG * kMergeRun];
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const float o0 = ordered(acc[c].x), o1 = ordered(acc[c].y), o2 = ordered(acc[c].z), o3 = ordered(acc[c].w);
-      if (active && r == 0) {
-        const unsigned lo = f32_to_f16_bits(zero ? 0.0f : o0 * iL) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o1 * iL) << 16);
-        const unsigned hi = f32_to_f16_bits(zero ? 0.0f : o2 * iL) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o3 * iL) << 16);
-        *reinterpret_cast<uint2*>(out_grp + (e40 + c) * 4) = make_uint2(lo, hi);
+      for (int k = 0; k < RPG * kMergeRun; ++k) {
+        const int sidx = gi * RPG * kMergeRun + k;
+        vq[k] = sidx < nsplit ? ld_state4<COHERENT>(pr, soff(sidx, hh) + ecol * 4) : v4f{0.0f, 0.0f, 0.0f, 0.0f};
       }
+      const bool ok = js < nsplit;
+      M = ok ? ml.x : kNegInf;
+      bd = ok && ml.y < 0.0f ? 1.0f : 0.0f;
+      M = fmaxf(M, dpp<0xB1>(M));   // quad_perm [1,0,3,2]
+      M = fmaxf(M, dpp<0x4E>(M));   // quad_perm [2,3,0,1]
+      M = fmaxf(M, dpp<0x141>(M));  // row_half_mirror
+      M = fmaxf(M, dpp<0x140>(M));  // row_mirror: every lane of a row holds the row's maximum
+      bd = fmaxf(bd, dpp<0xB1>(bd));
+      bd = fmaxf(bd, dpp<0x4E>(bd));
+      bd = fmaxf(bd, dpp<0x141>(bd));
+      bd = fmaxf(bd, dpp<0x140>(bd));
+      auto lane_f = [](float x, int l) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), l));
+      };
+      const float M0 = fmaxf(lane_f(M, 0), lane_f(M, 16)), M1 = fmaxf(lane_f(M, 32), lane_f(M, 48));
+      const float B0 = fmaxf(lane_f(bd, 0), lane_f(bd, 16)), B1 = fmaxf(lane_f(bd, 32), lane_f(bd, 48));
+      M = hb ? M1 : M0;
+      bd = hb ? B1 : B0;
+      const float Mref = (M == kNegInf) ? 0.0f : M;
+      v2f* wl = reinterpret_cast<v2f*>(lds) + wave * 64;  // (weight, l) of split j of half hb at hb * 32 + j
+      wl[lane] = v2f{ok ? ex2(ml.x - Mref) : 0.0f, ok ? ml.y : 0.0f};
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int rr = 0; rr < RPG; ++rr) {
+        const int r = gi * RPG + rr;
+        if (r < nrun) {
+          v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
+          float lacc = 0.0f;
+#pragma unroll
+          for (int u = 0; u < kMergeRun; ++u) {
+            const v2f wlv = wl[hb * 32 + r * kMergeRun + u];  // zero weight and l past nsplit
+            const v4f x = vq[rr * kMergeRun + u];
+            acc.x = __builtin_fmaf(wlv.x, x.x, acc.x);
+            acc.y = __builtin_fmaf(wlv.x, x.y, acc.y);
+            acc.z = __builtin_fmaf(wlv.x, x.z, acc.z);
+            acc.w = __builtin_fmaf(wlv.x, x.w, acc.w);
+            lacc = __builtin_fmaf(wlv.x, wlv.y, lacc);
+          }
+          *reinterpret_cast<v4f*>(rsum + r * GH * D + 4 * c) = acc;
+          if (c % (D / 4) == 0) rsumL[r * GH + h] = lacc;
+        }
+      }
+    }
+    __syncthreads();
+    if (gi == 0) {  // M and bd of this thread's head are this thread's own
+      v4f o = {0.0f, 0.0f, 0.0f, 0.0f};
+      float L = 0.0f;
+      for (int r = 0; r < nrun; ++r) {  // run sums added in run order, from zero
+        o += *reinterpret_cast<const v4f*>(rsum + r * GH * D + 4 * c);
+        L += rsumL[r * GH + h];
+      }
+      const bool zero = M == kNegInf || bd != 0.0f;
+      const float iL = 1.0f / L;  // one division per head, then products
+      const unsigned lo = f32_to_f16_bits(zero ? 0.0f : o.x * iL) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o.y * iL) << 16);
+      const unsigned hi = f32_to_f16_bits(zero ? 0.0f : o.z * iL) | ((unsigned)f32_to_f16_bits(zero ? 0.0f : o.w * iL) << 16);
+      *reinterpret_cast<uint2*>(out_grp + 4 * c) = make_uint2(lo, hi);
     }
     return;
   }
