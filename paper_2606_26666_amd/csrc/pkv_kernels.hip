@@ -69,8 +69,15 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t page_rsrc(const void* base, in
 
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+// Cache policy of the K and V page loads: non-temporal (the nt bit of the buffer
+// instruction's cache-policy operand). A step reads every KV byte once; with the
+// streaming hint the paged K/V pattern reads 7-9% faster on MI355X than with the default
+// policy (read-only probe of the decode's pages: B8 two-head tasks 75.8 -> 69.2 us, B1
+// 27.1 -> 25.5 us), while sc0 alone changes nothing.
+constexpr int kKvPolicy = 2;
+
+__device__ __forceinline__ uint4 kv_load16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kKvPolicy);
   return make_uint4(x.x, x.y, x.z, x.w);
 }
 
@@ -546,9 +553,9 @@ struct ValuTask {
     const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, page_bytes);
     const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, page_bytes);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) kr[i] = buffer_load16(kr_rsrc, lane_off_b, i * step_b);
+    for (int i = 0; i < 4; ++i) kr[i] = kv_load16(kr_rsrc, lane_off_b, i * step_b);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) vr[i] = buffer_load16(vr_rsrc, lane_off_b, i * step_b);
+    for (int i = 0; i < 4; ++i) vr[i] = kv_load16(vr_rsrc, lane_off_b, i * step_b);
   }
 
   // Both issues are unconditional (pages past the wave's count are not live), so every
@@ -821,9 +828,9 @@ struct MfmaTask {
     const __amdgpu_buffer_rsrc_t kr_rsrc = page_rsrc(a.k + (size_t)phys * page_stride, page_bytes);
     const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, page_bytes);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) kr[i] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, kv_off, i * 4 * tok_b, 0);
+    for (int i = 0; i < 4; ++i) kr[i] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, kv_off, i * 4 * tok_b, kKvPolicy);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, kv_off, i * 4 * tok_b, 0);
+    for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, kv_off, i * 4 * tok_b, kKvPolicy);
   }
 
   // Both issues are unconditional (pages past the wave's count are not live), so every
@@ -1794,9 +1801,9 @@ __global__ __launch_bounds__(W * 64) void page_read_kernel(PageReadArgs a) {
       const __amdgpu_buffer_rsrc_t vr_rsrc = page_rsrc(a.v + (size_t)phys * page_stride, bytes);
       const int kv_off = grp * tok_b + (g + hh) * D * 2 + col * 16;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kr[i] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, kv_off, i * 4 * tok_b, 0);
+      for (int i = 0; i < 4; ++i) kr[i] = __builtin_amdgcn_raw_buffer_load_b128(kr_rsrc, kv_off, i * 4 * tok_b, kKvPolicy);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, kv_off, i * 4 * tok_b, 0);
+      for (int i = 0; i < 4; ++i) vr[i] = __builtin_amdgcn_raw_buffer_load_b128(vr_rsrc, kv_off, i * 4 * tok_b, kKvPolicy);
     };
     auto fold = [&](const v4u (&kr)[4], const v4u (&vr)[4]) {
 #pragma unroll
