@@ -258,16 +258,17 @@ def measure(runner, steps, warmup, flush_bufs):
 
 
 def read_ceiling(pkv, torch, buf, sink, nbytes, reps=7):
-    """Streaming-read bandwidth (GB/s) of the first `nbytes` of the 1 GiB buffer, from the
-    read kernel's own execution interval (launch-stamped events), each read after a full
-    pass over the buffer so that the bytes read are not in the 256 MB last-level cache."""
+    """Streaming-read bandwidth (GB/s) of the first `nbytes` of the 1 GiB buffer with the
+    decode's K/V load policy (non-temporal loads), from the read kernel's own execution
+    interval (launch-stamped events), each read after a full pass over the buffer with
+    allocating loads, so that the bytes read are not in the 256 MB last-level cache."""
     Ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
     view = buf[:nbytes - nbytes % 16]
     us = []
     for _ in range(reps):
         pkv.pkv_stream_read(buf, sink)
         e0, e1 = Ev(), Ev()
-        pkv.pkv_stream_read(view, sink, events=(e0, e1))
+        pkv.pkv_stream_read_nt_timed(view, sink, events=(e0, e1))
         torch.cuda.synchronize()
         us.append(e0.elapsed_time(e1) * 1e3)
     return view.numel() / float(np.median(us)) / 1e3

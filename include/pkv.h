@@ -298,6 +298,13 @@ int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t s
 int pkv_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream,
                           hipEvent_t start, hipEvent_t stop);
 
+/* pkv_stream_read_timed with non-temporal loads, the cache policy of the decode kernel's
+ * K and V page loads (each KV byte is read once per step): the streaming-read ceiling
+ * for that policy. Arguments, errors and events as for pkv_stream_read_timed. Not meant
+ * for evicting the last-level cache: use pkv_stream_read, whose loads allocate. */
+int pkv_stream_read_nt_timed(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream,
+                             hipEvent_t start, hipEvent_t stop);
+
 /* Read-only probe of the decode kernel's KV access pattern (the read-bandwidth term of
  * the cost model, Sec. 3.5, measured for the paged layout of Sec. 3.2 instead of a
  * contiguous stream). For each of the first min(*num_tasks, max_tasks) records of

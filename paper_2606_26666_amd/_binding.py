@@ -74,6 +74,7 @@ _SIGS = {
     "pkv_stream_copy": (ctypes.c_int, [_P, _P, _SZ, _P]),
     "pkv_stream_read": (ctypes.c_int, [_P, _SZ, _P, _P]),
     "pkv_stream_read_timed": (ctypes.c_int, [_P, _SZ, _P, _P, _P, _P]),
+    "pkv_stream_read_nt_timed": (ctypes.c_int, [_P, _SZ, _P, _P, _P, _P]),
     "pkv_stream_read_pages": (ctypes.c_int, [_P, _P, _I32, _P, _I32, _I32, _I32, _I32, _P, _P, _I32, _I32, _P,
                                              _P, _P, _P]),
 }
@@ -318,6 +319,17 @@ def pkv_stream_read(src: torch.Tensor, sink: torch.Tensor, stream=None, events=N
         _check("pkv_stream_read", lib().pkv_stream_read(*args))
     else:
         _check("pkv_stream_read_timed", lib().pkv_stream_read_timed(*args, *_events(events)))
+
+
+def pkv_stream_read_nt_timed(src: torch.Tensor, sink: torch.Tensor, stream=None, events=None):
+    """Streaming read of `src` with non-temporal loads (the decode's K/V load policy);
+    events: optional (start, stop) stamped with the kernel's execution interval."""
+    if not (src.is_cuda and src.is_contiguous()):
+        raise TypeError("pkv_stream_read_nt_timed needs a contiguous device tensor")
+    n = src.numel() * src.element_size()
+    args = (src.data_ptr(), n - n % 16, _dev(sink, torch.int32, "sink"), _stream(stream))
+    ev = _events(events) if events is not None else (None, None)
+    _check("pkv_stream_read_nt_timed", lib().pkv_stream_read_nt_timed(*args, *ev))
 
 
 def pkv_stream_read_pages(k_cache: torch.Tensor, v_cache: torch.Tensor, block_table: torch.Tensor,

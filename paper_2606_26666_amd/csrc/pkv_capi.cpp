@@ -329,6 +329,12 @@ int pkv_stream_read_timed(const void* src, size_t bytes, uint32_t* sink, hipStre
   return from_hip(launch_read(src, bytes, sink, stream, start, stop));
 }
 
+int pkv_stream_read_nt_timed(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream, hipEvent_t start,
+                             hipEvent_t stop) {
+  if (!src || !sink || bytes % 16 != 0 || !aligned(src, 16) || !aligned(sink, 4)) return PKV_ERR_INVALID_ARG;
+  return from_hip(launch_read(src, bytes, sink, stream, start, stop, true));
+}
+
 int pkv_stream_read_pages(const uint16_t* k_cache, const uint16_t* v_cache, int32_t num_pages,
                           const int32_t* block_table, int32_t max_pages_per_row, int32_t B, int32_t Hkv, int32_t d,
                           const pkv_task* tasks, const int32_t* num_tasks, int32_t max_tasks,

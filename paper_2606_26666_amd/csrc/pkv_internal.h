@@ -98,6 +98,6 @@ struct PageReadArgs {
 hipError_t launch_page_read(const PageReadArgs& a, int heads_per_workgroup, hipStream_t s, hipEvent_t start,
                             hipEvent_t stop);
 hipError_t launch_read(const void* src, size_t bytes, unsigned* sink, hipStream_t s, hipEvent_t start = nullptr,
-                       hipEvent_t stop = nullptr);
+                       hipEvent_t stop = nullptr, bool non_temporal = false);
 
 }  // namespace pkv

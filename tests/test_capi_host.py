@@ -137,6 +137,8 @@ def test_copy_and_init_validation():
     assert L.pkv_stream_copy(0, FAKE, 16, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_stream_read(FAKE, 17, FAKE, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_stream_read(FAKE, 16, 0, None) == pkv.PKV_ERR_INVALID_ARG
+    assert L.pkv_stream_read_nt_timed(FAKE, 17, FAKE, None, None, None) == pkv.PKV_ERR_INVALID_ARG
+    assert L.pkv_stream_read_nt_timed(FAKE, 16, 0, None, None, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_workspace_init(FAKE, 100, 1, 8, None) == pkv.PKV_ERR_WORKSPACE
     assert L.pkv_workspace_init(0, 1 << 20, 1, 8, None) == pkv.PKV_ERR_INVALID_ARG
     assert L.pkv_check_device_status(0, None, None) == pkv.PKV_ERR_INVALID_ARG

@@ -49,3 +49,20 @@ def test_page_read_probe_skips_records_of_no_valid_plan():
         assert _probe(case, bufs, hpw, sink) > 0
     bufs.num_tasks.fill_(1 << 30)  # a count beyond the buffer is capped at max_tasks
     assert _probe(case, bufs, 1, sink) > 0
+
+
+def test_streaming_reads_both_policies():
+    """The contiguous streaming reads (allocating, and non-temporal as the decode's K/V
+    loads) read a buffer without changing it, write nothing but their sink word, and the
+    non-temporal one stamps its own execution interval."""
+    buf = torch.arange(1 << 20, dtype=torch.int32, device="cuda")
+    ref = buf.clone()
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pkv.pkv_stream_read(buf, sink)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    pkv.pkv_stream_read_nt_timed(buf, sink, events=(e0, e1))
+    pkv.pkv_stream_read_nt_timed(buf[:4], sink)  # one 16-byte load
+    torch.cuda.synchronize()
+    assert e0.elapsed_time(e1) > 0
+    assert torch.equal(buf, ref)
+    assert int(sink.item()) == 0  # the data does not hash to the sink's fixed value
