@@ -479,10 +479,6 @@ def oracle_step_tok_s(runner):
 
 CALIBRATION = os.path.join(ROOT, "paper_2606_26666_amd", "calibration_mi355x.json")
 # (workload, route, policy, task target) steps the cost model is fitted on: the split
-# sensitivity sweep of the one-launch workqueue plus every other route on the ragged
-# B8 trace and on B1 (exact buckets are left out: their step time includes host launch
-# time whenever the host falls behind)
-# (workload, route, policy, task target) steps the cost model is fitted on: the split
 # sensitivity sweep of the one-launch workqueue on B1 and B8 bimodal, the one-launch
 # route on the other traces, and every route of the bench's routes tables at the task
 # target of the cost model's rule (0) (exact buckets are left out: their step time
