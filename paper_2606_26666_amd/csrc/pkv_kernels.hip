@@ -1419,7 +1419,9 @@ __device__ __forceinline__ TaskRec plan_task(const PlanArgs& a, const PlanLds& L
 // token h0, h_pages pages) while wave 0 plans. Once the plan is in LDS (flag `ready`),
 // the verdict is the plan's t1 for this workgroup's first task (index `task`) if that
 // task is the hinted one (same row, KV head, first token and page count), else -1: the
-// run is dropped. dropped() looks without waiting; last_t1() waits for the plan.
+// run is dropped. Each wave forms it once, at the first check after the plan is in LDS
+// (in the page loop, overlapped with its loads). dropped() looks without waiting;
+// last_t1() waits for the plan and returns the verdict.
 struct SpecTask {
   const PlanArgs& pa;
   PlanLds PL;
@@ -1514,6 +1516,8 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   bool begun = false;  // the workgroup's body holds a task begun before the plan
   int plan_ntasks = 0;
   __shared__ int plan_ready;  // wave planner: set once wave 0 has put the plan in LDS
+  bool spec_kept = false;     // the speculative run was this workgroup's first task
+  int hr = 0, hg = 0, h0 = 0, h1 = 0;  // the hinted task (h1: the plan's t1 once kept)
   // The speculative run is for one-head workgroups: with KV-head pairs its extra live
   // state pushed the kernel past 256 registers per lane (spills in the page loop, 50%
   // slower on the B8 traces), so a pair's hinted task is only begun and primed.
@@ -1546,7 +1550,7 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
         hv[3] = ld_i32<true>(tp + 4);
       }
       const int n_raw = threadIdx.x < 64 ? wave_plan_len(a.plan) : 0;
-      const int hr = uniform(hv[0]), hg = uniform(hv[1]), h0 = uniform(hv[2]), h1 = uniform(hv[3]);
+      hr = uniform(hv[0]), hg = uniform(hv[1]), h0 = uniform(hv[2]), h1 = uniform(hv[3]);
       if (has_hint && hr >= 0 && hr < a.B && hg >= 0 && hg % NH == 0 && hg + NH <= a.Hkv && h0 >= 0 && h1 > h0 &&
           h1 <= a.max_pages_per_row * P) {
         body.begin(a, hr, hg, h0, h1);
@@ -1560,7 +1564,12 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       if (begun && kSpecRun) {
         SpecTask spec{a.plan, PL, &plan_ready, NH * (int)blockIdx.x, hr, hg, h0, (h1 + P - 1) / P};
         body.run(a, spec, lds);
-        // the run ended with a workgroup barrier: wave 0's plan is visible to every wave
+        // The run ended with a workgroup barrier: wave 0's plan is visible to every wave.
+        // Every wave's verdict is the same; most waves formed it in the page loop, so a
+        // kept run finishes with the hint's record and the plan's t1, no lookup.
+        const int t1 = spec.last_t1();
+        spec_kept = t1 >= 0;
+        if (spec_kept) h1 = t1;
       } else {
         __syncthreads();
       }
@@ -1588,7 +1597,14 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
       rec[3] = tp[4];
     }
   };
-  if (!PLAN || NH * (int)blockIdx.x < plan_ntasks) fetch(NH * (int)blockIdx.x);  // PLAN: only real tasks
+  if (spec_kept) {  // the plan's record of this workgroup's first task is the hint's
+    rec[0] = hr;
+    rec[1] = hg;
+    rec[2] = h0;
+    rec[3] = h1;
+  } else if (!PLAN || NH * (int)blockIdx.x < plan_ntasks) {
+    fetch(NH * (int)blockIdx.x);  // PLAN: only real tasks
+  }
   int ntasks = PLAN ? plan_ntasks : uniform(*a.num_tasks);
   if (ntasks > a.max_tasks) ntasks = a.max_tasks;
   // The end of task t (KV heads g .. g + NH - 1 of `row`): its partial state from the
@@ -1649,8 +1665,8 @@ __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   // task. NH = 2: the plan's task count is Hkv times its split count, and Hkv is even.
   int t = NH * (int)blockIdx.x;
   if (t + NH <= ntasks) {
-    if (begun && kSpecRun && body.covers(uniform(rec[0]), uniform(rec[1]), uniform(rec[2]), uniform(rec[3])))
-      finish(t, uniform(rec[0]), uniform(rec[1]));  // the speculative run was this task
+    if (spec_kept)
+      finish(t, hr, hg);  // the speculative run was this task
     else
       task(body, t, begun && !kSpecRun);  // a begun task that has not run keeps its loads if they cover t
   }
