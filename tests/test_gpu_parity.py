@@ -616,11 +616,11 @@ def test_plan_decode_one_split_per_long_row(target):
     assert pkv.pkv_check_device_status(bufs.ws) == 0
 
 
-# merge_group has three paths: every state of a head loaded by each thread (at most 32
-# splits), one block of states staged in LDS (33-64 splits), and several blocks after a
-# first pass for the maximum (more than 64). Rows of 282 and 375 tiles give every route
-# that merges 48, 128 or 200 splits, at every G; G = 1 and 2 stage their states in LDS
-# from 33 splits on.
+# merge_group has three paths: column threads over runs of states (at most 32 splits,
+# every G; covered by the full-size and ragged cases above), one block of states staged
+# in LDS (33-64 splits), and several blocks after a first pass for the maximum (more than
+# 64). Rows of 282 and 375 tiles give every route that merges 48, 128 or 200 splits, at
+# every G.
 MANY = [9000, 12000, 70, 0]
 
 
