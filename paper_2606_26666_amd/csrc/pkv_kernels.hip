@@ -150,13 +150,15 @@ __device__ __forceinline__ void st_state4(__amdgpu_buffer_rsrc_t r, int off, v4f
 // merge in the library goes through merge_group, so all routes round identically. A
 // (row, KV head) with a marked split (l < 0) is zeroed.
 //
-// Work: an item is one run of one float4 column of the output; each thread takes at
-// most kMergeItems items per round, so it keeps at most kMergeItems * kMergeRun float4
-// loads in flight (64 registers). The first round's loads are issued before the m/l
-// loads, so they travel during the maximum's exchange; with up to 64 splits and G = 4
-// one round covers every item of a 512-thread workgroup (two of a 256-thread one). A
-// state that does not exist is read at an offset past the end of the slot buffer, which
-// a buffer load returns as zero without touching memory, and gets weight 0.
+// Up to 32 splits (four runs) the column path below reads only existing states. Beyond
+// that, the general path: an item is one run of one float4 column of the output; each
+// thread takes at most kMergeItems items per round, so it keeps at most kMergeItems *
+// kMergeRun float4 loads in flight (64 registers). The first round's loads are issued
+// before the m/l loads, so they travel during the maximum's exchange; with up to 64
+// splits and G = 4 one round covers every item of a 512-thread workgroup (two of a
+// 256-thread one). There a state that does not exist is read at an offset past the end
+// of the slot buffer, which a buffer load returns as zero without touching memory, and
+// gets weight 0.
 constexpr int kMergeBlock = 64;  // split states whose m and l are staged in LDS at a time
 constexpr int kMergeRun = 8;     // splits per run
 constexpr int kRunsPerBlock = kMergeBlock / kMergeRun;
