@@ -287,10 +287,12 @@ const char* pkv_status_string(int status);
  * known traffic, used to calibrate HBM traffic counters. */
 int pkv_stream_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
-/* Streaming read of `bytes` (a multiple of 16) at src on `stream`: the read-bandwidth
- * probe (the paper's streaming-bandwidth calibration, Sec. 3.5) and a way to evict the
- * last-level cache with clean lines between timed steps. `sink` is a device word that
- * is written only if the data hashes to a fixed value. */
+/* Streaming read of `bytes` (a multiple of 16) at src on `stream`, with allocating
+ * (default-policy) loads: a read-bandwidth probe (the paper's streaming-bandwidth
+ * calibration, Sec. 3.5; pkv_stream_read_nt_timed measures it with the decode's load
+ * policy) and a way to evict the last-level cache with clean lines between timed
+ * steps. `sink` is a device word that is written only if the data hashes to a fixed
+ * value. */
 int pkv_stream_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t stream);
 
 /* pkv_stream_read with start/stop events stamped by the launch itself (the kernel's
