@@ -173,7 +173,7 @@ int pkv_decode_timed(const uint16_t* q, const uint16_t* k_cache, const uint16_t*
   if (!std::isfinite(sm_scale)) return PKV_ERR_INVALID_ARG;
   if (max_tasks < 1) return PKV_ERR_INVALID_ARG;
   if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, max_tasks)) return PKV_ERR_WORKSPACE;
-  if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
+  if ((int64_t)max_tasks * (int64_t)slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
                            Hkv, sm_scale, out, ws_layout(ws, B, Hkv));
   a.tasks = tasks;
@@ -215,7 +215,7 @@ int pkv_decode_rect(const uint16_t* q, const uint16_t* k_cache, const uint16_t* 
   const int32_t slots = pkv_max_tasks(rows, Hkv, S);
   if (slots < 0) return PKV_ERR_INVALID_ARG;
   if (ws_bytes < pkv_workspace_size(B, Hq, Hkv, d, slots)) return PKV_ERR_WORKSPACE;
-  if ((int64_t)slots * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
+  if ((int64_t)slots * (int64_t)slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
   DecodeArgs a = make_args(q, k_cache, v_cache, num_pages, block_table, max_pages_per_row, seq_lens, B, Hq,
                            Hkv, sm_scale, out, ws_layout(ws, B, Hkv));
   a.S = S;
@@ -379,8 +379,9 @@ int plan_decode(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_ca
   if ((st = make_plan_args(seq_lens, nullptr, B, max_pages_per_row, num_pages, params, tasks, max_tasks,
                            split_offsets, num_tasks, Scratch{nullptr, nullptr, nullptr}, &pa)) != PKV_OK)
     return st;
-  if ((int64_t)max_tasks * slot_floats(G) * 4 > (int64_t)slot_bytes) return PKV_ERR_WORKSPACE;
-  if ((int64_t)max_tasks * slot_floats(G) * 4 > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
+  const int64_t state_bytes = (int64_t)max_tasks * (int64_t)slot_floats(G) * 4;
+  if (state_bytes > (int64_t)slot_bytes) return PKV_ERR_WORKSPACE;
+  if (state_bytes > INT32_MAX) return PKV_ERR_INVALID_ARG;  // 32-bit slot offsets
   Scratch at{};
   if (sc) {
     at = *sc;
