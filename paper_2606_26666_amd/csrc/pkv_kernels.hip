@@ -290,9 +290,15 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     if (gi == 0) {  // M and bd of this thread's head are this thread's own
       v4f o = {0.0f, 0.0f, 0.0f, 0.0f};
       float L = 0.0f;
-      for (int r = 0; r < nrun; ++r) {  // run sums added in run order, from zero
-        o += *reinterpret_cast<const v4f*>(rsum + r * GH * D + 4 * c);
-        L += rsumL[r * GH + h];
+      // Run sums added in run order, from zero. All four runs' LDS reads go out together;
+      // a run past nrun adds +0, which leaves the sums bitwise unchanged (a sum started
+      // at +0 is never -0).
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const v4f v = *reinterpret_cast<const v4f*>(rsum + r * GH * D + 4 * c);
+        const float lr = rsumL[r * GH + h];
+        o += r < nrun ? v : v4f{0.0f, 0.0f, 0.0f, 0.0f};
+        L += r < nrun ? lr : 0.0f;
       }
       const bool zero = M == kNegInf || bd != 0.0f;
       const float iL = 1.0f / L;  // one division per head, then products
