@@ -8,8 +8,9 @@
 //
 // Work mapping. One workgroup owns one task: one KV head g of one row and a token
 // range [t0, t1). Its W = 8 wavefronts (two per SIMD, one workgroup per compute unit)
-// take the range's 16-token pages round-robin, two pages in flight per wave. Two task bodies: MfmaTask (G = 4, 8) forms Q.K^T and P.V on
-// the matrix cores; ValuTask (G = 1, 2) reads one page of one head as four 1 KiB loads
+// take the range's 16-token pages round-robin, two pages in flight per wave. Two task
+// bodies: MfmaTask (G = 4, 8) forms Q.K^T and P.V on the matrix cores; ValuTask (G = 1,
+// 2) reads one page of one head as four 1 KiB loads
 // (lane (r, c) = (lane/16, lane%16) loads 16 bytes, dims 8c..8c+7, of token 4i+r, so
 // every load covers four whole 256-byte head rows), forms partial dot products with
 // v_dot2_f32_f16 completed by a 16-lane DPP butterfly, and runs an online softmax per
@@ -150,15 +151,13 @@ __device__ __forceinline__ void st_state4(__amdgpu_buffer_rsrc_t r, int off, v4f
 // merge in the library goes through merge_group, so all routes round identically. A
 // (row, KV head) with a marked split (l < 0) is zeroed.
 //
-// Up to 32 splits (four runs) the column path below reads only existing states. Beyond
-// that, the general path: an item is one run of one float4 column of the output; each
+// Up to 64 splits (eight runs) the column path below reads only existing states. Beyond
+// that, the general path: a first pass over blocks of kMergeBlock states for the
+// maximum, then per block an item is one run of one float4 column of the output; each
 // thread takes at most kMergeItems items per round, so it keeps at most kMergeItems *
-// kMergeRun float4 loads in flight (64 registers). The first round's loads are issued
-// before the m/l loads, so they travel during the maximum's exchange; with up to 64
-// splits and G = 4 one round covers every item of a 512-thread workgroup (two of a
-// 256-thread one). There a state that does not exist is read at an offset past the end
-// of the slot buffer, which a buffer load returns as zero without touching memory, and
-// gets weight 0.
+// kMergeRun float4 loads in flight (64 registers). A state that does not exist is read
+// at an offset past the end of the slot buffer, which a buffer load returns as zero
+// without touching memory, and gets weight 0.
 constexpr int kMergeBlock = 64;  // split states whose m and l are staged in LDS at a time
 constexpr int kMergeRun = 8;     // splits per run
 constexpr int kRunsPerBlock = kMergeBlock / kMergeRun;
@@ -166,10 +165,15 @@ constexpr int kMergeItems = 2;   // (run, column) items per thread per round
 constexpr int kMaxMergeWaves = 16;
 constexpr int kOutOfRange = (int)0x80000000u;  // buffer offset past any slot buffer
 
-template <int G, int NH = 1>
+constexpr int kColRuns = 8;      // the column path merges up to kColRuns runs (64 splits)
+
+template <int G, int NH, int NT>
 constexpr int merge_lds_floats() {
   constexpr int GH = NH * G;
-  return 2 * kMergeBlock * GH + kRunsPerBlock * GH * D + kRunsPerBlock * GH + 2 * kMaxMergeWaves * GH + 3 * GH;
+  constexpr int general = 2 * kMergeBlock * GH + kRunsPerBlock * GH * D + kRunsPerBlock * GH +
+                          2 * kMaxMergeWaves * GH + 3 * GH;
+  constexpr int column = (NT / 64) * 256 + kColRuns * GH * D + kColRuns * GH;
+  return general > column ? general : column;
 }
 
 // The nsplit states at slots slot0 + s*stride (s < nsplit) of one (row, KV head) into
@@ -203,47 +207,65 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
   const int my_hh = myh / G, my_h = myh % G;
   auto soff = [&](int s, int hh) { return (slot0 + s * stride + hh) * SB; };
 
-  // At most four runs (32 splits): column path. Column thread c (< GH * D / 4) owns the
+  // At most eight runs (64 splits): column path. Column thread c (< GH * D / 4) owns the
   // four output elements 4c .. 4c + 3, so lanes 0-31 of a wave hold one query head's D
   // columns and lanes 32-63 the next head's (GH = 1: one head per half-wave). The NT
-  // threads form NG groups of column threads; group i sums runs i * RPG .. i * RPG +
-  // RPG - 1, each in split order from zero, reading its columns from every existing
-  // state of those runs (one 16-byte load per state, none for states that do not exist:
-  // 1 KiB per wave instruction). Lane j of a half loads (m, l) of split j of its half's
-  // head; the maximum and the marker are reduced over the half, and the weights pass
-  // through LDS, which every lane of the half reads at the same address. The run sums
-  // meet in LDS and group 0 adds them in run order, from zero. The operations and their
-  // order are those of the general path below (entries past nsplit in the last run add
-  // 0 * 0), so every path rounds alike.
-  if (nsplit <= 4 * kMergeRun) {
+  // threads form NG groups of column threads; group i sums runs i, i + NG, i + 2 NG, ...,
+  // each in split order from zero, reading its columns from every existing state of
+  // those runs (one 16-byte load per state, none for states that do not exist: 1 KiB
+  // per wave instruction). A round gives each group RR runs (two; four where one group
+  // covers every column): with four groups one round covers all eight runs, otherwise
+  // four (32 splits), and a merge of more splits takes a second round whose loads refill
+  // each run's registers as soon as they are consumed. Lane j of a half loads (m, l) of
+  // splits j and j + 32 of its half's head; the maximum and the marker are reduced over
+  // the half, and the weights pass through LDS, which every lane of the half reads at
+  // the same address. The run sums meet in LDS and group 0 adds them in run order, from
+  // zero. The operations and their order are those of the general path below (entries
+  // past nsplit in the last run add 0 * 0), so every path rounds alike.
+  if (nsplit <= kColRuns * kMergeRun) {
     constexpr int kColThreads = GH * D / 4;
     constexpr int NG = NT / kColThreads >= 4 ? 4 : NT / kColThreads;
-    constexpr int RPG = 4 / NG;                    // runs per group
+    constexpr int RR = NG == 1 ? 4 : 2;             // runs per group and round
+    constexpr int NRD = kColRuns / (NG * RR);       // rounds
     constexpr int kWaves = (NG * kColThreads + 63) / 64;
-    float* rsum = lds + kWaves * 128;              // [run][GH * D] run sums of acc
-    float* rsumL = rsum + 4 * GH * D;              // [run][GH] run sums of l
+    float* rsum = lds + kWaves * 256;               // [run][GH * D] run sums of acc
+    float* rsumL = rsum + kColRuns * GH * D;        // [run][GH] run sums of l
     static_assert(D == 128 && NT % kColThreads == 0 && (NG == 1 || NG == 2 || NG == 4), "column merge shape");
-    static_assert(kWaves * 128 + 4 * GH * D + 4 * GH <= merge_lds_floats<G, NH>(), "column merge LDS");
+    static_assert(NRD * NG * RR == kColRuns, "column merge rounds");
+    static_assert(kWaves * 256 + kColRuns * GH * D + kColRuns * GH <= merge_lds_floats<G, NH, NT>(),
+                  "column merge LDS");
     const int gi = tid / kColThreads;              // group
     const int c = tid - gi * kColThreads;          // column thread
     const int h = c / (D / 4);                     // query head within the GH merged
     const int nrun = (nsplit + kMergeRun - 1) / kMergeRun;
+    const bool wide = nsplit > 4 * kMergeRun;      // runs 4-7 exist
     float M = kNegInf, bd = 0.0f;
     if (gi < NG) {
       const int hb = lane >> 5, js = lane & 31;
       const int hh = h / G;                        // KV head within the NH merged
       const int ecol = (h % G) * D + (c % (D / 4)) * 4;  // first element in that KV head's acc
-      const int ml_off = js < nsplit ? soff(js, hh) + (G * D + 2 * (h % G)) * 4 : kOutOfRange;
-      const v2f ml = ld_state2<COHERENT>(pr, ml_off);
-      v4f vq[RPG * kMergeRun];
+      const int ml_at = (G * D + 2 * (h % G)) * 4;
+      const bool ok0 = js < nsplit, ok1 = wide && js + 32 < nsplit;
+      const v2f ml0 = ld_state2<COHERENT>(pr, ok0 ? soff(js, hh) + ml_at : kOutOfRange);
+      v2f ml1 = {0.0f, 0.0f};
+      if (wide) ml1 = ld_state2<COHERENT>(pr, ok1 ? soff(js + 32, hh) + ml_at : kOutOfRange);
+      // vq[k * kMergeRun + u]: split u of this group's run in slot k of the current round.
+      // A slot is refilled with the next round's run as soon as it has been consumed, so
+      // the rounds' loads overlap.
+      v4f vq[RR * kMergeRun];
+      auto issue = [&](int rd, int k) {  // run gi + NG * (rd * RR + k) into slot k
+        if (NG * (rd * RR + k) >= 4 && !wide) return;  // a run >= 4: none exists
 #pragma unroll
-      for (int k = 0; k < RPG * kMergeRun; ++k) {
-        const int sidx = gi * RPG * kMergeRun + k;
-        vq[k] = sidx < nsplit ? ld_state4<COHERENT>(pr, soff(sidx, hh) + ecol * 4) : v4f{0.0f, 0.0f, 0.0f, 0.0f};
-      }
-      const bool ok = js < nsplit;
-      M = ok ? ml.x : kNegInf;
-      bd = ok && ml.y < 0.0f ? 1.0f : 0.0f;
+        for (int u = 0; u < kMergeRun; ++u) {
+          const int sidx = (gi + NG * (rd * RR + k)) * kMergeRun + u;
+          vq[k * kMergeRun + u] =
+              sidx < nsplit ? ld_state4<COHERENT>(pr, soff(sidx, hh) + ecol * 4) : v4f{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+      };
+#pragma unroll
+      for (int k = 0; k < RR; ++k) issue(0, k);
+      M = fmaxf(ok0 ? ml0.x : kNegInf, ok1 ? ml1.x : kNegInf);
+      bd = (ok0 && ml0.y < 0.0f) || (ok1 && ml1.y < 0.0f) ? 1.0f : 0.0f;
       M = fmaxf(M, dpp<0xB1>(M));   // quad_perm [1,0,3,2]
       M = fmaxf(M, dpp<0x4E>(M));   // quad_perm [2,3,0,1]
       M = fmaxf(M, dpp<0x141>(M));  // row_half_mirror
@@ -260,29 +282,34 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
       M = hb ? M1 : M0;
       bd = hb ? B1 : B0;
       const float Mref = (M == kNegInf) ? 0.0f : M;
-      v2f* wl = reinterpret_cast<v2f*>(lds) + wave * 64;  // (weight, l) of split j of half hb at hb * 32 + j
-      wl[lane] = v2f{ok ? ex2(ml.x - Mref) : 0.0f, ok ? ml.y : 0.0f};
+      v2f* wl = reinterpret_cast<v2f*>(lds) + wave * 128;  // (weight, l) of split j of half hb at hb * 64 + j
+      wl[hb * 64 + js] = v2f{ok0 ? ex2(ml0.x - Mref) : 0.0f, ok0 ? ml0.y : 0.0f};
+      if (wide) wl[hb * 64 + 32 + js] = v2f{ok1 ? ex2(ml1.x - Mref) : 0.0f, ok1 ? ml1.y : 0.0f};
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-      for (int rr = 0; rr < RPG; ++rr) {
-        const int r = gi * RPG + rr;
-        if (r < nrun) {
-          v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
-          float lacc = 0.0f;
+      for (int rd = 0; rd < NRD; ++rd) {
 #pragma unroll
-          for (int u = 0; u < kMergeRun; ++u) {
-            const v2f wlv = wl[hb * 32 + r * kMergeRun + u];  // zero weight and l past nsplit
-            const v4f x = vq[rr * kMergeRun + u];
-            acc.x = __builtin_fmaf(wlv.x, x.x, acc.x);
-            acc.y = __builtin_fmaf(wlv.x, x.y, acc.y);
-            acc.z = __builtin_fmaf(wlv.x, x.z, acc.z);
-            acc.w = __builtin_fmaf(wlv.x, x.w, acc.w);
-            lacc = __builtin_fmaf(wlv.x, wlv.y, lacc);
+        for (int k = 0; k < RR; ++k) {
+          const int r = gi + NG * (rd * RR + k);
+          if (r < nrun) {
+            v4f acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            float lacc = 0.0f;
+#pragma unroll
+            for (int u = 0; u < kMergeRun; ++u) {
+              const v2f wlv = wl[hb * 64 + r * kMergeRun + u];  // zero weight and l past nsplit
+              const v4f x = vq[k * kMergeRun + u];
+              acc.x = __builtin_fmaf(wlv.x, x.x, acc.x);
+              acc.y = __builtin_fmaf(wlv.x, x.y, acc.y);
+              acc.z = __builtin_fmaf(wlv.x, x.z, acc.z);
+              acc.w = __builtin_fmaf(wlv.x, x.w, acc.w);
+              lacc = __builtin_fmaf(wlv.x, wlv.y, lacc);
+            }
+            *reinterpret_cast<v4f*>(rsum + r * GH * D + 4 * c) = acc;
+            if (c % (D / 4) == 0) rsumL[r * GH + h] = lacc;
           }
-          *reinterpret_cast<v4f*>(rsum + r * GH * D + 4 * c) = acc;
-          if (c % (D / 4) == 0) rsumL[r * GH + h] = lacc;
+          if (rd + 1 < NRD) issue(rd + 1, k);  // refill the slot just consumed
         }
       }
     }
@@ -290,15 +317,18 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     if (gi == 0) {  // M and bd of this thread's head are this thread's own
       v4f o = {0.0f, 0.0f, 0.0f, 0.0f};
       float L = 0.0f;
-      // Run sums added in run order, from zero. All four runs' LDS reads go out together;
-      // a run past nrun adds +0, which leaves the sums bitwise unchanged (a sum started
-      // at +0 is never -0).
+      // Run sums added in run order, from zero, four runs' LDS reads at a time; a run
+      // past nrun adds +0, which leaves the sums bitwise unchanged (a sum started at +0
+      // is never -0).
+      for (int r0 = 0; r0 < nrun; r0 += 4) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const v4f v = *reinterpret_cast<const v4f*>(rsum + r * GH * D + 4 * c);
-        const float lr = rsumL[r * GH + h];
-        o += r < nrun ? v : v4f{0.0f, 0.0f, 0.0f, 0.0f};
-        L += r < nrun ? lr : 0.0f;
+        for (int k = 0; k < 4; ++k) {
+          const int r = r0 + k;
+          const v4f v = *reinterpret_cast<const v4f*>(rsum + r * GH * D + 4 * c);
+          const float lr = rsumL[r * GH + h];
+          o += r < nrun ? v : v4f{0.0f, 0.0f, 0.0f, 0.0f};
+          L += r < nrun ? lr : 0.0f;
+        }
       }
       const bool zero = M == kNegInf || bd != 0.0f;
       const float iL = 1.0f / L;  // one division per head, then products
@@ -357,12 +387,9 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     sBad[tid] = 0.0f;
     sL[tid] = 0.0f;
   }
-  const bool one_block = nsplit <= kMergeBlock;
-  if (!one_block) {  // pass 1: maximum over every block first
-    for (int s0 = 0; s0 < nsplit; s0 += kMergeBlock) {
-      load_ml(s0, min(kMergeBlock, nsplit - s0));
-      reduce_max();
-    }
+  for (int s0 = 0; s0 < nsplit; s0 += kMergeBlock) {  // pass 1: maximum over every block
+    load_ml(s0, min(kMergeBlock, nsplit - s0));
+    reduce_max();
   }
   float A[EPT];
 #pragma unroll
@@ -405,9 +432,8 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
     };
     __syncthreads();  // the previous block's LDS is consumed
 #pragma unroll
-    for (int j = 0; j < kMergeItems; ++j) issue(j, tid + j * NT);  // in flight during the max
+    for (int j = 0; j < kMergeItems; ++j) issue(j, tid + j * NT);  // in flight during the weights
     load_ml(s0, cnt);
-    if (one_block) reduce_max();
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
       const int e = tid + k * NT;
@@ -1505,7 +1531,7 @@ template <int G, int W, bool FUSED, bool PLAN, int NH = 1>
 __global__ __launch_bounds__(W * 64) void split_kernel(DecodeArgs a) {
   static_assert(NH == 1 || (NH == 2 && FUSED && PLAN), "head pairs run on the one-launch route");
   __shared__ float lds[lds_floats<G, W, NH>()];
-  __shared__ float lds_merge[FUSED ? merge_lds_floats<G, NH>() : 1];
+  __shared__ float lds_merge[FUSED ? merge_lds_floats<G, NH, W * 64>() : 1];
   __shared__ int lds_last;
   __shared__ int p_len[PLAN ? kMaxFusedPlanBatch : 1];
   __shared__ int p_off[PLAN ? kMaxFusedPlanBatch + 1 : 1];
@@ -1728,7 +1754,7 @@ constexpr int kMergeThreads = 256;
 
 template <int G, bool RECT>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(DecodeArgs a) {
-  __shared__ float lds[merge_lds_floats<G>()];
+  __shared__ float lds[merge_lds_floats<G, 1, kMergeThreads>()];
   const int j = blockIdx.x / a.Hkv;  // the launch's row index
   const int g = blockIdx.x % a.Hkv;
   const int row = (RECT && a.n_rows > 0) ? a.row_ids[j] : j;

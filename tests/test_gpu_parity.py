@@ -616,11 +616,12 @@ def test_plan_decode_one_split_per_long_row(target):
     assert pkv.pkv_check_device_status(bufs.ws) == 0
 
 
-# merge_group has three paths: column threads over runs of states (at most 32 splits,
-# every G; covered by the full-size and ragged cases above), one block of states staged
-# in LDS (33-64 splits), and several blocks after a first pass for the maximum (more than
-# 64). Rows of 282 and 375 tiles give every route that merges 48, 128 or 200 splits, at
-# every G.
+# merge_group has two paths: column threads over runs of states (at most 64 splits, in
+# one round of loads up to 32 splits and two beyond; the full-size and ragged cases above
+# take the first round only), and blocks of states staged in LDS after a first pass for
+# the maximum (more than 64). Rows of 282 and 375 tiles give every route that merges 48,
+# 128 or 200 splits, at every G; the fused and two-kernel merges lay the column path out
+# differently (512 against 256 threads), so their bitwise equality checks it as well.
 MANY = [9000, 12000, 70, 0]
 
 
