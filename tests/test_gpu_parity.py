@@ -619,16 +619,17 @@ def test_plan_decode_one_split_per_long_row(target):
 # merge_group has two paths: column threads over runs of states (at most 64 splits, in
 # one round of loads up to 32 splits and two beyond; the full-size and ragged cases above
 # take the first round only), and blocks of states staged in LDS after a first pass for
-# the maximum (more than 64). Rows of 282 and 375 tiles give every route that merges 48,
-# 128 or 200 splits, at every G; the fused and two-kernel merges lay the column path out
+# the maximum (more than 64). Rows of 282 and 375 tiles give every route that merges 33
+# to 200 splits, at every G; the fused and two-kernel merges lay the column path out
 # differently (512 against 256 threads), so their bitwise equality checks it as well.
 MANY = [9000, 12000, 70, 0]
 
 
-@pytest.mark.parametrize("split_max", [48, 128, 200])
+@pytest.mark.parametrize("split_max", [33, 48, 64, 65, 128, 200])
 @pytest.mark.parametrize("hq,hkv", [(8, 8), (16, 8), (32, 8), (32, 4)])
 def test_merge_of_many_splits(hq, hkv, split_max):
-    """Split counts 48, 128 and 200 (policy 0, S = split_max): the fused and two-kernel
+    """Split counts 33 to 200 (policy 0, S = split_max; 33 and 64 bound the column
+    path's second round, 65 is the general path's smallest): the fused and two-kernel
     merges are bitwise equal and within tolerance of the oracle, and the one-launch route
     (KV-head pairs at G = 4, whose merge covers both heads' states) is bitwise the same."""
     case = Case(MANY, hq=hq, hkv=hkv, seed=61)
