@@ -213,10 +213,13 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
   // threads form NG groups of column threads; group i sums runs i, i + NG, i + 2 NG, ...,
   // each in split order from zero, reading its columns from every existing state of
   // those runs (one 16-byte load per state, none for states that do not exist: 1 KiB
-  // per wave instruction). A round gives each group RR runs (two; four where one group
-  // covers every column): with four groups one round covers all eight runs, otherwise
-  // four (32 splits), and a merge of more splits takes a second round whose loads refill
-  // each run's registers as soon as they are consumed. Lane j of a half loads (m, l) of
+  // per wave instruction). A round gives each group RR runs, four where one group covers
+  // every column or two groups cover one KV head (32 float4 loads in flight per thread),
+  // else two: with four groups, or two for one KV head, one round covers all eight runs;
+  // otherwise a round covers four (32 splits), and a merge of more splits takes a second
+  // round whose loads refill each run's registers as soon as they are consumed (two
+  // groups for a KV-head pair keep 16 loads per thread, within the pair kernel's
+  // registers). Lane j of a half loads (m, l) of
   // splits j and j + 32 of its half's head; the maximum and the marker are reduced over
   // the half, and the weights pass through LDS, which every lane of the half reads at
   // the same address. The run sums meet in LDS and group 0 adds them in run order, from
@@ -225,7 +228,7 @@ __device__ __forceinline__ void merge_group(__amdgpu_buffer_rsrc_t pr, int slot0
   if (nsplit <= kColRuns * kMergeRun) {
     constexpr int kColThreads = GH * D / 4;
     constexpr int NG = NT / kColThreads >= 4 ? 4 : NT / kColThreads;
-    constexpr int RR = NG == 1 ? 4 : 2;             // runs per group and round
+    constexpr int RR = NG == 1 || (NG == 2 && NH == 1) ? 4 : 2;  // runs per group and round
     constexpr int NRD = kColRuns / (NG * RR);       // rounds
     constexpr int kWaves = (NG * kColThreads + 63) / 64;
     float* rsum = lds + kWaves * 256;               // [run][GH * D] run sums of acc
